@@ -1,0 +1,399 @@
+"""Pins of the CPU oracle against facts fixed by the paper and by mathematics.
+
+Each test checks the oracle against something other than itself: library
+routines for special cases, exact rational arithmetic, brute force on tiny
+inputs, closed forms, and the invariants the paper states (stateless,
+deterministic experts, §2.1 and §5.1; shadows carry the primary's weights,
+§5.3; the MoE output is the gate-weighted sum of the selected experts, §2.1).
+"""
+import itertools
+from fractions import Fraction
+
+import numpy as np
+import pytest
+import scipy.special
+import torch
+
+from oracle import moe_ew as O
+from paper_2601_01310_amd import synth
+from tests._util import bf16_bits_to_f32, host, u16, ulp_diff_bf16
+
+RNG = np.random.default_rng(12345)
+
+
+def rand_bf16(shape, scale=1.0, rng=RNG):
+    return O.f64_to_bf16(rng.standard_normal(shape) * scale)
+
+
+# ---------------------------------------------------------------- bf16 rounding
+
+
+def test_bf16_widen_then_round_is_identity():
+    bits = np.arange(0, 1 << 16, dtype=np.uint32).astype(np.uint16)
+    f = bf16_bits_to_f32(bits)
+    finite = np.isfinite(f)
+    back = O.f64_to_bf16(O.bf16_to_f64(bits[finite]))
+    assert np.array_equal(back, bits[finite])
+
+
+def test_bf16_rounding_matches_torch_on_float32_values():
+    # torch rounds float32 -> bfloat16 to nearest-even: a library routine that
+    # must agree with the oracle on every float32-representable input.
+    rng = np.random.default_rng(7)
+    v = np.concatenate([
+        rng.standard_normal(200000).astype(np.float32),
+        (rng.standard_normal(20000) * 1e-39).astype(np.float32),  # subnormals
+        # exact bf16 midpoints: a bf16 value plus half its spacing
+        (bf16_bits_to_f32(rng.integers(0x0080, 0x7F00, 20000).astype(np.uint16)).view(np.uint32)
+         + np.uint32(0x8000)).view(np.float32),
+    ])
+    ref = u16(torch.from_numpy(v).to(torch.bfloat16))
+    got = O.f64_to_bf16(v.astype(np.float64))
+    assert np.array_equal(got, ref)
+
+
+def test_bf16_rounds_once_from_float64():
+    # 1 + 2^-8 + 2^-40 lies above the midpoint between 1 and 1 + 2^-7, so it
+    # rounds up; a detour through float32 would drop 2^-40 and round to even.
+    cases = {
+        1.0 + 2.0 ** -8 + 2.0 ** -40: 0x3F81,
+        1.0 + 2.0 ** -8: 0x3F80,          # tie -> even
+        1.0 + 3 * 2.0 ** -8: 0x3F82,      # tie -> even
+        -0.0: 0x8000,
+        2.0 ** -133: 0x0001,              # smallest subnormal
+        3.0 * 2.0 ** -134: 0x0002,        # subnormal tie -> even
+        float("inf"): 0x7F80,
+        -1e39: 0xFF80,
+    }
+    for v, want in cases.items():
+        assert int(O.f64_to_bf16(np.array([v]))[0]) == want, v
+
+
+# ---------------------------------------------------------------- gate logits
+
+
+def _exact_to_f32(fr: Fraction) -> np.float32:
+    """Nearest float32 to a rational, ties to even (by exact comparison)."""
+    c = np.float32(float(fr))
+    best = None
+    for cand in (np.nextafter(c, np.float32(-np.inf)), c, np.nextafter(c, np.float32(np.inf))):
+        dist = abs(Fraction(float(cand)) - fr)
+        key = (dist, int(np.array(cand).view(np.uint32)) & 1)
+        if best is None or key < best[0]:
+            best = (key, cand)
+    return best[1]
+
+
+def test_gate_logits_are_correctly_rounded_exact_dot_products():
+    T, E, d = 6, 5, 97
+    x = rand_bf16((T, d))
+    wg = rand_bf16((E, d), 0.02)
+    got = O.gate_logits(x, wg)
+    xf, wf = O.bf16_to_f64(x), O.bf16_to_f64(wg)
+    for t in range(T):
+        for e in range(E):
+            exact = sum(Fraction(float(a)) * Fraction(float(b)) for a, b in zip(xf[t], wf[e]))
+            assert got[t, e] == _exact_to_f32(exact)
+
+
+def test_gate_logits_one_hot_picks_a_weight_column():
+    d, E = 64, 8
+    wg = rand_bf16((E, d), 0.02)
+    x = np.zeros((d, d), np.uint16)
+    x[np.arange(d), np.arange(d)] = 0x3F80  # bf16 1.0
+    got = O.gate_logits(x, wg)
+    assert np.array_equal(got, bf16_bits_to_f32(wg).T)
+
+
+# ---------------------------------------------------------------- top-k and weights
+
+
+@pytest.mark.parametrize("E,k", [(6, 1), (6, 2), (6, 6), (8, 2), (16, 8)])
+def test_topk_matches_brute_force_with_ties(E, k):
+    rng = np.random.default_rng(E * 10 + k)
+    logits = rng.integers(-3, 4, size=(300, E)).astype(np.float32)  # many ties
+    got = O.topk(logits, k)
+    for t in range(logits.shape[0]):
+        want = sorted(range(E), key=lambda e: (-float(logits[t, e]), e))[:k]
+        assert list(got[t]) == want
+
+
+def test_topk_orders_by_float32_not_by_rounding_of_probabilities():
+    # two logits one float32 ulp apart must be ordered, even though their
+    # probabilities would be equal after float32 rounding of the softmax
+    a = np.float32(1.0)
+    b = np.nextafter(a, np.float32(2.0))
+    got = O.topk(np.array([[a, b, -5.0]], np.float32), 2)
+    assert list(got[0]) == [1, 0]
+
+
+def test_gate_weights_sum_to_one_and_match_topk_softmax():
+    rng = np.random.default_rng(3)
+    logits = rng.standard_normal((500, 256)).astype(np.float32)
+    ids = O.topk(logits, 8)
+    w = O.gate_weights(logits, ids)
+    assert np.allclose(w.sum(axis=1), 1.0, atol=1e-12, rtol=0)
+    # softmax over all E renormalised over the chosen k == softmax over the chosen logits
+    chosen = np.take_along_axis(logits.astype(np.float64), ids.astype(np.int64), axis=1)
+    assert np.allclose(w, scipy.special.softmax(chosen, axis=1), atol=1e-14, rtol=0)
+    assert np.all(np.diff(w, axis=1) <= 0)  # larger logit first -> non-increasing weights
+
+
+def test_gate_weights_special_cases():
+    logits = np.array([[0.5, 2.0, 2.0, -1.0]], np.float32)
+    ids = O.topk(logits, 1)
+    assert O.gate_weights(logits, ids)[0, 0] == 1.0
+    ids2 = O.topk(logits, 2)
+    assert list(ids2[0]) == [1, 2]
+    assert list(O.gate_weights(logits, ids2)[0]) == [0.5, 0.5]
+
+
+# ---------------------------------------------------------------- remap
+
+
+def _tables():
+    # E=6 logical experts; this EW holds experts 0..3 as slots 0..3 and shadows
+    # of experts 1 and 3 as slots 4, 5; experts 4, 5 live elsewhere.
+    ert = np.full((6, 2), -1, np.int32)
+    ert[:4, 0] = np.arange(4)
+    ert[1, 1] = 4
+    ert[3, 1] = 5
+    return ert
+
+
+def test_remap_all_alive_uses_primaries_and_skips_remote_experts():
+    ert = _tables()
+    rng = np.random.default_rng(0)
+    ids = np.stack([rng.permutation(6)[:3] for _ in range(50)]).astype(np.int32)
+    ps, nu = O.remap(ids, ert, np.ones(6, np.uint8))
+    want = np.where(ids < 4, ids, -1)
+    assert np.array_equal(ps, want) and nu == 0
+
+
+def test_remap_dead_primary_moves_exactly_its_pairs_to_the_shadow():
+    ert = _tables()
+    rng = np.random.default_rng(1)
+    ids = np.stack([rng.permutation(6)[:3] for _ in range(80)]).astype(np.int32)
+    alive = np.ones(6, np.uint8)
+    base, _ = O.remap(ids, ert, alive)
+    alive[3] = 0
+    ps, nu = O.remap(ids, ert, alive)
+    assert nu == 0
+    assert np.array_equal(ps[ids == 3], np.full((ids == 3).sum(), 5))
+    assert np.array_equal(ps[ids != 3], base[ids != 3])
+
+
+def test_remap_no_live_candidate_counts_unserved():
+    ert = _tables()
+    ids = np.array([[0, 1, 4], [2, 0, 5], [1, 3, 0]], np.int32)
+    alive = np.ones(6, np.uint8)
+    alive[[0, 1, 4]] = 0  # expert 0 has no replica; expert 1 loses both
+    ps, nu = O.remap(ids, ert, alive)
+    assert nu == 5  # experts 0 and 1 have local candidates, none alive: 2 + 1 + 2 pairs
+    assert ps.tolist() == [[-1, -1, -1], [2, -1, -1], [-1, 3, -1]]
+
+
+def test_remap_ignores_out_of_range_table_entries():
+    ert = np.array([[7, 1], [-5, -1]], np.int32)  # slot 7 does not exist (S=2)
+    ps, nu = O.remap(np.array([[0, 1]], np.int32), ert, np.ones(2, np.uint8))
+    assert ps.tolist() == [[1, -1]] and nu == 0
+
+
+# ---------------------------------------------------------------- dispatch
+
+
+def test_dispatch_matches_stable_sort_construction():
+    rng = np.random.default_rng(4)
+    T, k, S = 300, 4, 7
+    ps = rng.integers(-1, S, size=(T, k)).astype(np.int32)
+    counts, offsets, perm, pair_row = O.dispatch(ps, S)
+    flat = ps.ravel()
+    assert np.array_equal(counts, np.bincount(flat[flat >= 0], minlength=S))
+    assert offsets[0] == 0 and np.array_equal(np.diff(offsets), counts)
+    keyed = np.flatnonzero(flat >= 0)
+    want = keyed[np.argsort(flat[keyed], kind="stable")]  # (slot, token, rank) order
+    assert np.array_equal(perm, want)
+    inv = np.full(T * k, -1)
+    inv[perm] = np.arange(len(perm))
+    assert np.array_equal(pair_row.ravel(), inv)
+
+
+def test_dispatch_empty():
+    counts, offsets, perm, pair_row = O.dispatch(np.full((5, 2), -1, np.int32), 3)
+    assert counts.tolist() == [0, 0, 0] and offsets.tolist() == [0, 0, 0, 0]
+    assert perm.size == 0 and (pair_row == -1).all()
+
+
+# ---------------------------------------------------------------- expert FFN closed forms
+
+
+def test_swiglu_closed_form_with_identity_and_permutation_weights():
+    # W1 = I, W3 = 2I, W2 = a permutation: h = bf16(silu(x) * 2x) and y[c] = h[pi(c)].
+    # Swapping the gate and up halves, or transposing W2, changes the result.
+    n = 32
+    rng = np.random.default_rng(5)
+    one, two = 0x3F80, 0x4000
+    w13 = np.zeros((2 * n, n), np.uint16)
+    w13[np.arange(n), np.arange(n)] = one
+    w13[n + np.arange(n), np.arange(n)] = two
+    pi = rng.permutation(n)
+    w2 = np.zeros((n, n), np.uint16)
+    w2[np.arange(n), pi] = one
+    x = rand_bf16((40, n), 2.0, rng)
+    h, y = O.expert_ffn(x, w13, w2)
+    xf = O.bf16_to_f64(x)
+    want_h = O.f64_to_bf16(xf * scipy.special.expit(xf) * 2.0 * xf)
+    assert np.array_equal(h, want_h)
+    assert np.array_equal(y, h[:, pi])
+
+
+def test_ffn_rows_are_independent_and_w2_scaling_is_exact():
+    rng = np.random.default_rng(6)
+    d, I = 64, 96
+    x = rand_bf16((9, d), 1.0, rng)
+    w13 = rand_bf16((2 * I, d), 0.05, rng)
+    w2 = rand_bf16((d, I), 0.05, rng)
+    h, y = O.expert_ffn(x, w13, w2)
+    for r in range(x.shape[0]):  # a row's result does not depend on its batch
+        hr, yr = O.expert_ffn(x[r:r + 1], w13, w2)
+        assert np.array_equal(hr[0], h[r]) and np.array_equal(yr[0], y[r])
+    w2x2 = O.f64_to_bf16(O.bf16_to_f64(w2) * 2.0)
+    _, y2 = O.expert_ffn(x, w13, w2x2)
+    assert np.array_equal(O.bf16_to_f64(y2), 2.0 * O.bf16_to_f64(y))
+
+
+def test_ffn_float64_agrees_with_float32_torch_within_bf16_rounding():
+    rng = np.random.default_rng(8)
+    d, I = 128, 256
+    x = rand_bf16((16, d), 1.0, rng)
+    w13 = rand_bf16((2 * I, d), 0.02 * 4, rng)
+    w2 = rand_bf16((d, I), 0.02 * 4, rng)
+    _, y = O.expert_ffn(x, w13, w2)
+    xt = torch.from_numpy(bf16_bits_to_f32(x))
+    wt = torch.from_numpy(bf16_bits_to_f32(w13))
+    g, uu = xt @ wt[:I].T, xt @ wt[I:].T
+    ht = (torch.nn.functional.silu(g) * uu).to(torch.bfloat16).float()
+    yt = (ht @ torch.from_numpy(bf16_bits_to_f32(w2)).T).to(torch.bfloat16)
+    assert ulp_diff_bf16(u16(yt), y).max() <= 2
+
+
+# ---------------------------------------------------------------- whole forward
+
+
+def _np_workload(wl):
+    return dict(x=host(wl.x), wg=None if wl.wg is None else host(wl.wg),
+                logits=None if wl.logits is None else host(wl.logits), k=wl.k,
+                ert=host(wl.ert), alive=host(wl.alive), w13=host(wl.w13), w2=host(wl.w2))
+
+
+@pytest.fixture(scope="module")
+def tiny():
+    return synth.make("tiny")
+
+
+def test_dense_mixture_brute_force_tiny(tiny):
+    """out[t] = sum over ALL experts e of g~_e * FFN_e(x_t), g~ = renormalised
+    gate weight on the top-k and 0 elsewhere (§2.1), evaluated densely with
+    torch float64 on every (token, expert) pair and no routing tables."""
+    a = _np_workload(tiny)
+    r = O.ew_forward(**a)
+    x = torch.from_numpy(bf16_bits_to_f32(a["x"]).astype(np.float64))
+    wg = torch.from_numpy(bf16_bits_to_f32(a["wg"]).astype(np.float64))
+    logits = (x @ wg.T).float()
+    T, E, k, I = tiny.T, tiny.E, tiny.k, tiny.I
+    p = torch.softmax(logits.double(), dim=1)
+    out = torch.zeros(T, tiny.d, dtype=torch.float64)
+    for t in range(T):
+        chosen = sorted(range(E), key=lambda e: (-float(logits[t, e]), e))[:k]
+        z = sum(float(p[t, e]) for e in chosen)
+        for e in range(E):  # dense: every expert, gate weight 0 off the top-k
+            gw = float(p[t, e]) / z if e in chosen else 0.0
+            w13 = torch.from_numpy(bf16_bits_to_f32(a["w13"][e]).astype(np.float64))
+            w2 = torch.from_numpy(bf16_bits_to_f32(a["w2"][e]).astype(np.float64))
+            g, u = w13[:I] @ x[t], w13[I:] @ x[t]
+            h = torch.from_numpy(bf16_bits_to_f32(O.f64_to_bf16(
+                (torch.nn.functional.silu(g) * u).numpy())).astype(np.float64))
+            y = torch.from_numpy(bf16_bits_to_f32(O.f64_to_bf16((w2 @ h).numpy())).astype(np.float64))
+            out[t] += gw * y
+    want = O.f64_to_bf16(out.numpy())
+    assert ulp_diff_bf16(r["out"], want).max() <= 1
+    assert (ulp_diff_bf16(r["out"], want) == 0).mean() > 0.99
+
+
+def test_failure_run_equals_no_failure_run_bitwise(tiny):
+    """Rerouting expert 3 to its shadow (same weights, §5.3) leaves every
+    output bit unchanged (replay through a healthy replica is identical, §5.1)."""
+    a = _np_workload(tiny)
+    r0 = O.ew_forward(**a)
+    a["alive"] = host(tiny.alive_after_failure())
+    r1 = O.ew_forward(**a)
+    assert np.array_equal(r0["out"], r1["out"])
+    assert np.array_equal(r0["ids"], r1["ids"])
+    moved = r0["ids"] == 3
+    assert (r1["pair_slot"][moved] == 9).all() and (r0["pair_slot"][moved] == 3).all()
+    assert r1["counts"][3] == 0 and r1["counts"][9] == r0["counts"][3]
+    assert r0["counts"].sum() == r1["counts"].sum() == tiny.T * tiny.k
+
+
+def test_token_permutation_permutes_outputs(tiny):
+    a = _np_workload(tiny)
+    r0 = O.ew_forward(**a)
+    pi = np.random.default_rng(9).permutation(tiny.T)
+    a["x"] = a["x"][pi]
+    r1 = O.ew_forward(**a)
+    assert np.array_equal(r1["out"], r0["out"][pi])
+    assert np.array_equal(r1["ids"], r0["ids"][pi])
+
+
+def test_unserved_pairs_are_dropped_without_renormalising(tiny):
+    a = _np_workload(tiny)
+    r0 = O.ew_forward(**a)
+    a["alive"] = a["alive"].copy()
+    a["alive"][[1, 9]] = 0  # expert 1 has no shadow; kill slot 9 too (expert 3's shadow)
+    r1 = O.ew_forward(**a)
+    assert r1["n_unserved"] == int((r0["ids"] == 1).sum())
+    t = np.flatnonzero((r0["ids"] == 1).any(axis=1))[0]
+    j_keep = [j for j in range(tiny.k) if r0["ids"][t, j] != 1]
+    y0 = O.bf16_to_f64(r0["y"][r0["pair_row"][t, j_keep]])
+    want = O.f64_to_bf16((r0["w"][t, j_keep][:, None] * y0).sum(axis=0))
+    assert np.array_equal(r1["out"][t], want)
+
+
+def test_partial_combines_over_expert_shares_add_up():
+    """Each EW of an expert-parallel group sums only its local pairs with the
+    global weights; summing the partials of all shares gives the full MoE
+    output (within the bf16 rounding of each partial)."""
+    E, n_share = 16, 4
+    wl = synth.make_custom(T=24, d=64, E=E, k=4, I=96, n_local=E, shadow_experts=[],
+                           gate="weights", seed=11)
+    a = _np_workload(wl)
+    full = O.ew_forward(**a)
+    acc = np.zeros((wl.T, wl.d))
+    for sh in range(n_share):
+        local = list(range(sh * 4, sh * 4 + 4))
+        ert = np.full((E, 2), -1, np.int32)
+        ert[local, 0] = np.arange(4)
+        b = dict(a, ert=ert, alive=np.ones(4, np.uint8), w13=a["w13"][local], w2=a["w2"][local])
+        part = O.ew_forward(**b)
+        assert part["n_unserved"] == 0
+        acc += O.bf16_to_f64(part["out"])
+    full_f = O.bf16_to_f64(full["out"])
+    assert np.all(np.abs(acc - full_f) <= 4 * 2.0 ** -8 * np.maximum(np.abs(full_f), 1e-3) + 1e-6)
+
+
+def test_sampled_token_path_equals_full_forward(tiny):
+    a = _np_workload(tiny)
+    r = O.ew_forward(**a)
+    toks = [0, 5, 17, 63]
+    ids, w, ps, out = O.ew_forward_tokens(toks, a["x"], a["wg"], a["logits"], a["k"], a["ert"],
+                                          a["alive"], lambda s: a["w13"][s], lambda s: a["w2"][s])
+    assert np.array_equal(ids, r["ids"][toks]) and np.array_equal(ps, r["pair_slot"][toks])
+    assert np.array_equal(out, r["out"][toks])
+
+
+def test_skewed_workload_sends_about_forty_percent_to_the_four_hottest():
+    wl = synth.make("dsv3_skew", with_weights=False)
+    ids = O.topk(host(wl.logits), wl.k)
+    local = ids[ids < 32]
+    share = np.isin(local, wl.hot_experts).mean()
+    assert 0.38 <= share <= 0.42, share
