@@ -1,0 +1,165 @@
+"""Benchmark: routed token-expert pairs per second of the EW forward on one GPU.
+
+One step is one tg_ew_forward call (gating, ERT remap and dispatch, grouped
+SwiGLU expert FFN, combine) over the Mixtral-shaped workload: T=4096 tokens,
+d=4096, E=8 experts, top-2, I=14336, 8 primary + 2 shadow slots, synthetic
+bf16 inputs already resident in HBM. Prints one JSON line.
+
+  python bench.py [--gpus 1] [--steps 20] [--warmup 3] [--workload mixtral]
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+STAGES = ["gate", "dispatch", "ffn_gateup", "ffn_down", "combine"]
+
+
+class HipEvents:
+    """hipEvent_t handles through the HIP runtime's C API (timing only)."""
+
+    def __init__(self):
+        self.hip = ctypes.CDLL("libamdhip64.so")
+        self.hip.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        self.hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p,
+                                                 ctypes.c_void_p]
+        self.hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+
+    def create(self, n):
+        out = []
+        for _ in range(n):
+            ev = ctypes.c_void_p()
+            if self.hip.hipEventCreate(ctypes.byref(ev)) != 0:
+                raise RuntimeError("hipEventCreate failed")
+            out.append(ev.value)
+        return out
+
+    def elapsed_ms(self, a, b):
+        ms = ctypes.c_float()
+        if self.hip.hipEventElapsedTime(ctypes.byref(ms), ctypes.c_void_p(a), ctypes.c_void_p(b)) != 0:
+            raise RuntimeError("hipEventElapsedTime failed")
+        return ms.value
+
+    def destroy(self, evs):
+        for e in evs:
+            self.hip.hipEventDestroy(ctypes.c_void_p(e))
+
+
+def cpu_baseline(wl, n_tokens: int = 96):
+    """The CPU oracle, as it stands, on a bounded sample of the workload:
+    the full forward of ``n_tokens`` seeded tokens (their routed pairs)."""
+    import numpy as np
+    import torch
+    from threadpoolctl import threadpool_info
+
+    from oracle import moe_ew as O
+
+    def host(t):
+        t = t.detach().cpu().contiguous()
+        return t.view(torch.int16).numpy().view(np.uint16) if t.dtype == torch.bfloat16 else t.numpy()
+
+    x, ert, alive = host(wl.x), host(wl.ert), host(wl.alive)
+    wg = None if wl.wg is None else host(wl.wg)
+    logits = None if wl.logits is None else host(wl.logits)
+    w13 = [host(wl.w13[s]) for s in range(wl.S)]
+    w2 = [host(wl.w2[s]) for s in range(wl.S)]
+    toks = sorted(np.random.default_rng(0).choice(wl.T, size=n_tokens, replace=False).tolist())
+    t0 = time.perf_counter()
+    _, _, ps, _ = O.ew_forward_tokens(toks, x, wg, logits, wl.k, ert, alive,
+                                      lambda s: w13[s], lambda s: w2[s])
+    dt = time.perf_counter() - t0
+    pairs = int((ps >= 0).sum())
+    threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    return {"value": pairs / dt, "unit": "routed pairs/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{n_tokens} seeded tokens of the workload ({pairs} routed pairs), float64 "
+                      f"per-token oracle incl. widening the touched slots' bf16 weights; {dt:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="mixtral")
+    ap.add_argument("--failover", action="store_true",
+                    help="time the run with the workload's failed primaries rerouted to shadows")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the expert-parallel "
+              "exchange across GPUs is not part of this build", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2601_01310_amd import synth, tg
+
+    tg.load()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    wl = synth.make(args.workload, device=dev)
+    alive = wl.alive_after_failure() if args.failover else wl.alive
+    f = tg.EwForward(wl, alive)
+    hip = HipEvents()
+    stream = torch.cuda.current_stream()
+
+    for _ in range(args.warmup):
+        f(stream)
+    evs = hip.create(6 * args.steps)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        tg.tg_ew_forward_timed(f.args, f.ws, f.ws_bytes, evs[6 * i:6 * i + 6], stream)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    stage_ms = [0.0] * 5
+    for i in range(args.steps):
+        e = evs[6 * i:6 * i + 6]
+        for j in range(5):
+            stage_ms[j] += hip.elapsed_ms(e[j], e[j + 1]) / args.steps
+    hip.destroy(evs)
+
+    ms = (t1 - t0) * 1e3 / args.steps
+    P = int(f.slot_offsets[-1])
+    d, I = wl.d, wl.I
+    gemm1_flop = 4.0 * d * I * P
+    gemm1_tflops = gemm1_flop / (stage_ms[2] * 1e-3) / 1e12
+    ffn_tflops = 6.0 * d * I * P / ((stage_ms[2] + stage_ms[3]) * 1e-3) / 1e12
+    line = {
+        "metric": "routed token-expert pairs/sec for EW forward",
+        "value": P / (ms * 1e-3),
+        "unit": "pairs/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"{args.workload}: T={wl.T} d={d} E={wl.E} top-{wl.k} I={I} "
+                               f"slots={wl.S}" + (" failover" if args.failover else ""),
+                   "routed_pairs": P},
+        "roofline": {"bound": "mfma", "kernel": "grouped_gemm gate/up + SwiGLU",
+                     "achieved": gemm1_tflops, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": gemm1_tflops / PEAK_BF16_TFLOPS, "traffic": None},
+        "stages_ms": dict(zip(STAGES, stage_ms)),
+        "expert_ffn_tflops": ffn_tflops,
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(wl)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

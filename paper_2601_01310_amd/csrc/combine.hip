@@ -1,0 +1,61 @@
+// Gate-weighted combine (§2.1): out[t] = bf16(sum_j w[t,j] * y[pair_row[t,j]])
+// in float32, in rank order j = 0..k-1, skipping pairs not routed here.
+// One block per token; each thread owns 8-element (16-byte) column chunks,
+// so the y rows are read and the output row written fully coalesced.
+#include "tg_device.h"
+#include "tg_launch.h"
+
+namespace tg {
+namespace {
+
+constexpr int kBlock = 256;
+
+__global__ __launch_bounds__(kBlock) void combine_kernel(const uint4* __restrict__ y,
+                                                         const int32_t* __restrict__ pair_row,
+                                                         const float* __restrict__ w, int T, int k,
+                                                         int nch, uint4* __restrict__ out) {
+  __shared__ int rows[32];
+  __shared__ float ws[32];
+  const int t = blockIdx.x;
+  if (threadIdx.x < k) {
+    rows[threadIdx.x] = pair_row[(size_t)t * k + threadIdx.x];
+    ws[threadIdx.x] = w[(size_t)t * k + threadIdx.x];
+  }
+  __syncthreads();
+  for (int c = threadIdx.x; c < nch; c += kBlock) {
+    float acc[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) acc[i] = 0.0f;
+    for (int j = 0; j < k; ++j) {
+      const int r = rows[j];
+      if (r < 0) continue;
+      const float wj = ws[j];
+      const uint4 v = y[(size_t)r * nch + c];
+      const uint32_t u[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        acc[2 * i] = fmaf(wj, __uint_as_float(u[i] << 16), acc[2 * i]);
+        acc[2 * i + 1] = fmaf(wj, __uint_as_float(u[i] & 0xffff0000u), acc[2 * i + 1]);
+      }
+    }
+    uint4 o;
+    o.x = pack_bf16x2(acc[0], acc[1]);
+    o.y = pack_bf16x2(acc[2], acc[3]);
+    o.z = pack_bf16x2(acc[4], acc[5]);
+    o.w = pack_bf16x2(acc[6], acc[7]);
+    out[(size_t)t * nch + c] = o;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_combine(const uint16_t* y, const int32_t* pair_row, const float* w, int T, int k,
+                          int d, uint16_t* out, hipStream_t stream) {
+  if (T == 0) return hipSuccess;
+  hipLaunchKernelGGL(combine_kernel, dim3(T), dim3(kBlock), 0, stream,
+                     reinterpret_cast<const uint4*>(y), pair_row, w, T, k, d / 8,
+                     reinterpret_cast<uint4*>(out));
+  return hipGetLastError();
+}
+
+}  // namespace tg

@@ -1,0 +1,216 @@
+// ERT remap with failure mask, per-slot counts, deterministic permutation and
+// the activation gather (§4.2, §5.1, §5.3; per-expert batching, §2.2.1).
+//
+// Three passes over the routed pairs, all integer and free of ordering races:
+//   1. remap_count: per pair, the first live candidate slot of its expert;
+//      per chunk of pairs, an S-wide histogram and an unserved count
+//      (integer LDS atomics: the totals do not depend on their order);
+//   2. scan: per-slot totals, exclusive slot offsets, and the base row of
+//      every (chunk, slot) in chunk order;
+//   3. scatter: each wave walks its quarter of a chunk in pair order and
+//      ranks equal slots with ballots, so rows follow (slot, token, rank).
+// The gather then copies one activation row per routed pair with 16-byte
+// loads and stores (rows are contiguous in source and destination, so the
+// copy is fully coalesced without staging).
+#include "tg_device.h"
+#include "tg_launch.h"
+
+namespace tg {
+namespace {
+
+constexpr int kMaxS = 1024;
+constexpr int kBlock = 256;
+
+__global__ __launch_bounds__(kBlock) void remap_count_kernel(
+    const int32_t* __restrict__ ids, int npairs, const int32_t* __restrict__ ert, int E, int R,
+    const uint8_t* __restrict__ alive, int S, int32_t* __restrict__ pair_slot,
+    int32_t* __restrict__ hist, int32_t* __restrict__ unserved_chunk) {
+  __shared__ int h[kMaxS];
+  __shared__ int nu;
+  for (int s = threadIdx.x; s < S; s += kBlock) h[s] = 0;
+  if (threadIdx.x == 0) nu = 0;
+  __syncthreads();
+  const int base = blockIdx.x * kDispatchChunk;
+  for (int i = threadIdx.x; i < kDispatchChunk; i += kBlock) {
+    const int p = base + i;
+    if (p >= npairs) break;
+    const int e = ids[p];
+    int slot = -1;
+    bool listed = false;
+    if (e >= 0 && e < E) {
+      for (int r = 0; r < R; ++r) {
+        const int c = ert[(size_t)e * R + r];
+        if (c >= 0 && c < S) {
+          listed = true;
+          if (alive[c]) {
+            slot = c;
+            break;
+          }
+        }
+      }
+    }
+    pair_slot[p] = slot;
+    if (slot >= 0)
+      atomicAdd(&h[slot], 1);
+    else if (listed)
+      atomicAdd(&nu, 1);
+  }
+  __syncthreads();
+  for (int s = threadIdx.x; s < S; s += kBlock) hist[(size_t)blockIdx.x * S + s] = h[s];
+  if (threadIdx.x == 0) unserved_chunk[blockIdx.x] = nu;
+}
+
+// One block of 1024 threads; thread s owns slot s.
+__global__ __launch_bounds__(1024) void scan_kernel(int32_t* __restrict__ hist,
+                                                    const int32_t* __restrict__ unserved_chunk,
+                                                    int nchunks, int S, int32_t* __restrict__ counts,
+                                                    int32_t* __restrict__ offsets,
+                                                    int32_t* __restrict__ n_unserved) {
+  __shared__ int sc[2][1024];
+  __shared__ int nu;
+  const int s = threadIdx.x;
+  if (s == 0) nu = 0;
+  int total = 0;
+  if (s < S) {
+    for (int c = 0; c < nchunks; ++c) {
+      const int v = hist[(size_t)c * S + s];
+      hist[(size_t)c * S + s] = total;  // base within the slot, made absolute below
+      total += v;
+    }
+  }
+  int part = 0;
+  for (int c = s; c < nchunks; c += 1024) part += unserved_chunk[c];
+  sc[0][s] = (s < S) ? total : 0;
+  __syncthreads();
+  if (part) atomicAdd(&nu, part);
+  // Hillis-Steele inclusive scan over the slot totals.
+  int cur = 0;
+  for (int off = 1; off < 1024; off <<= 1) {
+    const int v = sc[cur][s] + (s >= off ? sc[cur][s - off] : 0);
+    sc[cur ^ 1][s] = v;
+    cur ^= 1;
+    __syncthreads();
+  }
+  const int incl = sc[cur][s];
+  const int excl = incl - ((s < S) ? total : 0);
+  if (s < S) {
+    counts[s] = total;
+    offsets[s] = excl;
+    for (int c = 0; c < nchunks; ++c) hist[(size_t)c * S + s] += excl;
+  }
+  if (s == S - 1) offsets[S] = incl;
+  __syncthreads();
+  if (s == 0) n_unserved[0] = nu;
+}
+
+__global__ __launch_bounds__(kBlock) void scatter_kernel(const int32_t* __restrict__ pair_slot,
+                                                         int npairs, int S,
+                                                         const int32_t* __restrict__ base,
+                                                         int32_t* __restrict__ perm,
+                                                         int32_t* __restrict__ pair_row) {
+  constexpr int kWaves = kBlock / kWave;
+  constexpr int kQuarter = kDispatchChunk / kWaves;
+  __shared__ int cnt[kWaves][kMaxS];
+  const int wave = threadIdx.x / kWave;
+  const int lane = lane_id();
+  for (int i = threadIdx.x; i < kWaves * kMaxS; i += kBlock) (&cnt[0][0])[i] = 0;
+  __syncthreads();
+  const int p0 = blockIdx.x * kDispatchChunk + wave * kQuarter;
+  for (int i = lane; i < kQuarter; i += kWave) {
+    const int p = p0 + i;
+    if (p < npairs) {
+      const int s = pair_slot[p];
+      if (s >= 0) atomicAdd(&cnt[wave][s], 1);
+    }
+  }
+  __syncthreads();
+  for (int s = threadIdx.x; s < S; s += kBlock) {
+    int run = base[(size_t)blockIdx.x * S + s];
+    for (int w = 0; w < kWaves; ++w) {
+      const int v = cnt[w][s];
+      cnt[w][s] = run;
+      run += v;
+    }
+  }
+  __syncthreads();
+  const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  for (int g = 0; g < kQuarter; g += kWave) {
+    const int p = p0 + g + lane;
+    int s = -1;
+    if (p < npairs) {
+      s = pair_slot[p];
+      if (s < 0) pair_row[p] = -1;
+    }
+    uint64_t active = __ballot(s >= 0);
+    while (active) {
+      const int leader = __builtin_ctzll(active);
+      const int sl = __shfl(s, leader);
+      const uint64_t m = __ballot(s == sl) & active;
+      const int start = cnt[wave][sl];
+      if (s == sl) {
+        const int row = start + __builtin_popcountll(m & lt);
+        perm[row] = p;
+        pair_row[p] = row;
+      }
+      if (lane == leader) cnt[wave][sl] = start + __builtin_popcountll(m);
+      active &= ~m;
+    }
+  }
+}
+
+__global__ __launch_bounds__(kBlock) void gather_kernel(const uint4* __restrict__ x,
+                                                        const int32_t* __restrict__ perm,
+                                                        const int32_t* __restrict__ offsets, int S,
+                                                        int k, int nch, uint4* __restrict__ x_perm) {
+  const int P = offsets[S];
+  const long total = (long)P * nch;
+  for (long q = (long)blockIdx.x * kBlock + threadIdx.x; q < total; q += (long)gridDim.x * kBlock) {
+    const int r = (int)(q / nch);
+    const int c = (int)(q - (long)r * nch);
+    const int t = perm[r] / k;
+    x_perm[q] = x[(size_t)t * nch + c];
+  }
+}
+
+}  // namespace
+
+size_t dispatch_workspace_bytes(int T, int k, int S) {
+  const size_t npairs = (size_t)T * k;
+  const size_t nchunks = (npairs + kDispatchChunk - 1) / kDispatchChunk;
+  const size_t hist = nchunks * (size_t)S * sizeof(int32_t);
+  return ((hist + 255) & ~(size_t)255) + ((nchunks * sizeof(int32_t) + 255) & ~(size_t)255) + 256;
+}
+
+hipError_t launch_remap_dispatch(const int32_t* ids, int T, int k, const int32_t* ert, int E, int R,
+                                 const uint8_t* alive, int S, const uint16_t* x, int d,
+                                 int32_t* pair_slot, int32_t* counts, int32_t* offsets,
+                                 int32_t* perm, int32_t* pair_row, uint16_t* x_perm,
+                                 int32_t* n_unserved, void* ws, hipStream_t stream) {
+  const int npairs = T * k;
+  const int nchunks = (npairs + kDispatchChunk - 1) / kDispatchChunk;
+  const size_t hist_bytes = ((size_t)nchunks * S * sizeof(int32_t) + 255) & ~(size_t)255;
+  int32_t* hist = static_cast<int32_t*>(ws);
+  int32_t* unserved_chunk = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + hist_bytes);
+  if (nchunks > 0) {
+    hipLaunchKernelGGL(remap_count_kernel, dim3(nchunks), dim3(kBlock), 0, stream, ids, npairs, ert,
+                       E, R, alive, S, pair_slot, hist, unserved_chunk);
+  }
+  hipLaunchKernelGGL(scan_kernel, dim3(1), dim3(1024), 0, stream, hist, unserved_chunk, nchunks, S,
+                     counts, offsets, n_unserved);
+  if (nchunks > 0) {
+    hipLaunchKernelGGL(scatter_kernel, dim3(nchunks), dim3(kBlock), 0, stream, pair_slot, npairs, S,
+                       hist, perm, pair_row);
+    if (x_perm) {
+      const int nch = d / 8;
+      const long maxq = (long)npairs * nch;
+      const long blocks = (maxq + kBlock - 1) / kBlock;
+      const int grid = (int)(blocks < 8192 ? blocks : 8192);
+      hipLaunchKernelGGL(gather_kernel, dim3(grid), dim3(kBlock), 0, stream,
+                         reinterpret_cast<const uint4*>(x), perm, offsets, S, k, nch,
+                         reinterpret_cast<uint4*>(x_perm));
+    }
+  }
+  return hipGetLastError();
+}
+
+}  // namespace tg

@@ -1,0 +1,284 @@
+// C ABI of libtg.so: argument validation, workspace layout and launch order.
+// Nothing here computes on the data; every step runs in the HIP kernels.
+#include <hip/hip_runtime.h>
+
+#include <cstdarg>
+#include <cstdio>
+#include <string>
+
+#include "tg.h"
+#include "tg_launch.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+tg_status fail(tg_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return s;
+}
+
+tg_status ok() {
+  g_last_error.clear();
+  return TG_OK;
+}
+
+tg_status hip_status(hipError_t e, const char* where) {
+  if (e != hipSuccess) return fail(TG_ERR_HIP, "%s: %s", where, hipGetErrorString(e));
+  return ok();
+}
+
+constexpr int kMaxK = 32, kMaxE = 1024, kMaxS = 1024, kMaxR = 16;
+
+tg_status check_gate_dims(int T, int E, int k) {
+  if (T < 0) return fail(TG_ERR_BAD_DIM, "T=%d must be >= 0", T);
+  if (E <= 0 || k <= 0) return fail(TG_ERR_BAD_DIM, "E=%d and k=%d must be > 0", E, k);
+  if (k > E) return fail(TG_ERR_BAD_DIM, "k=%d exceeds E=%d", k, E);
+  if (k > kMaxK) return fail(TG_ERR_UNSUPPORTED, "k=%d exceeds %d", k, kMaxK);
+  if (E > kMaxE) return fail(TG_ERR_UNSUPPORTED, "E=%d exceeds %d", E, kMaxE);
+  if ((long long)T * k >= (1LL << 31)) return fail(TG_ERR_UNSUPPORTED, "T*k >= 2^31");
+  return TG_OK;
+}
+
+tg_status check_hidden(int d, const char* name) {
+  if (d <= 0) return fail(TG_ERR_BAD_DIM, "%s=%d must be > 0", name, d);
+  if (d % 256) return fail(TG_ERR_UNSUPPORTED, "%s=%d is not a multiple of 256", name, d);
+  return TG_OK;
+}
+
+tg_status check_inter(int I) {
+  if (I <= 0) return fail(TG_ERR_BAD_DIM, "I=%d must be > 0", I);
+  if (I % 128) return fail(TG_ERR_UNSUPPORTED, "I=%d is not a multiple of 128", I);
+  return TG_OK;
+}
+
+tg_status check_slots(int S, int R) {
+  if (S <= 0 || R <= 0) return fail(TG_ERR_BAD_DIM, "S=%d and R=%d must be > 0", S, R);
+  if (S > kMaxS) return fail(TG_ERR_UNSUPPORTED, "S=%d exceeds %d", S, kMaxS);
+  if (R > kMaxR) return fail(TG_ERR_UNSUPPORTED, "R=%d exceeds %d", R, kMaxR);
+  return TG_OK;
+}
+
+size_t align256(size_t b) { return (b + 255) & ~(size_t)255; }
+
+// Carves the tg_ew_forward workspace; with base == nullptr only sizes it.
+struct EwLayout {
+  int32_t* ids;
+  float* w;
+  int32_t* pair_slot;
+  int32_t* counts;
+  int32_t* offsets;
+  int32_t* pair_row;
+  int32_t* n_unserved;
+  int32_t* perm;
+  void* dispatch_ws;
+  uint16_t* x_perm;
+  uint16_t* h;
+  uint16_t* y;
+  size_t bytes;
+};
+
+EwLayout ew_layout(const tg_ew_args* a, char* base) {
+  EwLayout L{};
+  size_t off = 0;
+  const size_t np = (size_t)a->T * a->k;
+  auto take = [&](size_t bytes) -> char* {
+    char* p = base ? base + off : nullptr;
+    off += align256(bytes);
+    return p;
+  };
+  L.ids = reinterpret_cast<int32_t*>(take(np * 4));
+  L.w = reinterpret_cast<float*>(take(np * 4));
+  L.pair_slot = reinterpret_cast<int32_t*>(take(np * 4));
+  L.counts = reinterpret_cast<int32_t*>(take((size_t)a->S * 4));
+  L.offsets = reinterpret_cast<int32_t*>(take(((size_t)a->S + 1) * 4));
+  L.pair_row = reinterpret_cast<int32_t*>(take(np * 4));
+  L.n_unserved = reinterpret_cast<int32_t*>(take(4));
+  L.perm = reinterpret_cast<int32_t*>(take(np * 4));
+  L.dispatch_ws = take(tg::dispatch_workspace_bytes(a->T, a->k, a->S));
+  L.x_perm = reinterpret_cast<uint16_t*>(take(np * a->d * 2));
+  L.h = reinterpret_cast<uint16_t*>(take(np * a->I * 2));
+  L.y = reinterpret_cast<uint16_t*>(take(np * a->d * 2));
+  L.bytes = off;
+  return L;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* tg_status_string(tg_status s) {
+  switch (s) {
+    case TG_OK: return "TG_OK";
+    case TG_ERR_NULL_ARG: return "TG_ERR_NULL_ARG";
+    case TG_ERR_BAD_DIM: return "TG_ERR_BAD_DIM";
+    case TG_ERR_UNSUPPORTED: return "TG_ERR_UNSUPPORTED";
+    case TG_ERR_WORKSPACE: return "TG_ERR_WORKSPACE";
+    case TG_ERR_HIP: return "TG_ERR_HIP";
+  }
+  return "TG_ERR_UNKNOWN";
+}
+
+const char* tg_last_error(void) { return g_last_error.c_str(); }
+
+tg_status tg_gate_topk(const uint16_t* x, const uint16_t* w_gate, const float* logits_in, int T,
+                       int d, int E, int k, float* logits_out, int32_t* topk_ids, float* topk_w,
+                       void* stream) {
+  tg_status st = check_gate_dims(T, E, k);
+  if (st != TG_OK) return st;
+  const bool weights_mode = (x != nullptr || w_gate != nullptr);
+  if (weights_mode) {
+    if (!x || !w_gate || logits_in)
+      return fail(TG_ERR_NULL_ARG, "give either x and w_gate, or logits_in");
+    if ((st = check_hidden(d, "d")) != TG_OK) return st;
+  } else if (!logits_in) {
+    return fail(TG_ERR_NULL_ARG, "give either x and w_gate, or logits_in");
+  }
+  if (!topk_ids || !topk_w) return fail(TG_ERR_NULL_ARG, "topk_ids and topk_w are required");
+  return hip_status(tg::launch_gate_topk(x, w_gate, logits_in, T, d, E, k,
+                                         weights_mode ? logits_out : nullptr, topk_ids, topk_w,
+                                         static_cast<hipStream_t>(stream)),
+                    "tg_gate_topk");
+}
+
+size_t tg_remap_dispatch_workspace(int T, int k, int S) {
+  if (T < 0 || k <= 0 || S <= 0) return 0;
+  return tg::dispatch_workspace_bytes(T, k, S);
+}
+
+tg_status tg_remap_dispatch(const int32_t* topk_ids, int T, int k, const int32_t* ert, int E,
+                            int R, const uint8_t* slot_alive, int S, const uint16_t* x, int d,
+                            int32_t* pair_slot, int32_t* slot_counts, int32_t* slot_offsets,
+                            int32_t* perm, int32_t* pair_row, uint16_t* x_perm,
+                            int32_t* n_unserved, void* ws, size_t ws_bytes, void* stream) {
+  tg_status st = check_gate_dims(T, E, k);
+  if (st != TG_OK) return st;
+  if ((st = check_slots(S, R)) != TG_OK) return st;
+  if (!topk_ids || !ert || !slot_alive || !pair_slot || !slot_counts || !slot_offsets || !perm ||
+      !pair_row || !n_unserved)
+    return fail(TG_ERR_NULL_ARG, "a required pointer is NULL");
+  if ((x == nullptr) != (x_perm == nullptr))
+    return fail(TG_ERR_NULL_ARG, "x and x_perm must both be given or both be NULL");
+  if (x_perm && (st = check_hidden(d, "d")) != TG_OK) return st;
+  const size_t need = tg::dispatch_workspace_bytes(T, k, S);
+  if (!ws || ws_bytes < need)
+    return fail(TG_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need, ws_bytes);
+  if (reinterpret_cast<uintptr_t>(ws) & 255)
+    return fail(TG_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  return hip_status(tg::launch_remap_dispatch(topk_ids, T, k, ert, E, R, slot_alive, S, x, d,
+                                              pair_slot, slot_counts, slot_offsets, perm, pair_row,
+                                              x_perm, n_unserved, ws,
+                                              static_cast<hipStream_t>(stream)),
+                    "tg_remap_dispatch");
+}
+
+tg_status tg_expert_ffn_grouped(const uint16_t* x_perm, const int32_t* slot_offsets, int S,
+                                int max_rows, const uint16_t* w13, const uint16_t* w2, int d,
+                                int I, uint16_t* h, uint16_t* y, void* stream) {
+  tg_status st;
+  if (S <= 0) return fail(TG_ERR_BAD_DIM, "S=%d must be > 0", S);
+  if (S > kMaxS) return fail(TG_ERR_UNSUPPORTED, "S=%d exceeds %d", S, kMaxS);
+  if (max_rows < 0) return fail(TG_ERR_BAD_DIM, "max_rows=%d must be >= 0", max_rows);
+  if ((st = check_hidden(d, "d")) != TG_OK) return st;
+  if ((st = check_inter(I)) != TG_OK) return st;
+  if (!x_perm || !slot_offsets || !w13 || !w2 || !h || !y)
+    return fail(TG_ERR_NULL_ARG, "a required pointer is NULL");
+  return hip_status(tg::launch_expert_ffn(x_perm, slot_offsets, S, max_rows, w13, w2, d, I, h, y,
+                                          static_cast<hipStream_t>(stream)),
+                    "tg_expert_ffn_grouped");
+}
+
+tg_status tg_combine(const uint16_t* y, const int32_t* pair_row, const float* topk_w, int T, int k,
+                     int d, uint16_t* out, void* stream) {
+  tg_status st;
+  if (T < 0 || k <= 0) return fail(TG_ERR_BAD_DIM, "T=%d >= 0 and k=%d > 0 required", T, k);
+  if (k > kMaxK) return fail(TG_ERR_UNSUPPORTED, "k=%d exceeds %d", k, kMaxK);
+  if ((st = check_hidden(d, "d")) != TG_OK) return st;
+  if (!y || !pair_row || !topk_w || !out) return fail(TG_ERR_NULL_ARG, "a required pointer is NULL");
+  return hip_status(
+      tg::launch_combine(y, pair_row, topk_w, T, k, d, out, static_cast<hipStream_t>(stream)),
+      "tg_combine");
+}
+
+static tg_status check_ew(const tg_ew_args* a) {
+  if (!a) return fail(TG_ERR_NULL_ARG, "args is NULL");
+  tg_status st = check_gate_dims(a->T, a->E, a->k);
+  if (st != TG_OK) return st;
+  if ((st = check_hidden(a->d, "d")) != TG_OK) return st;
+  if ((st = check_inter(a->I)) != TG_OK) return st;
+  if ((st = check_slots(a->S, a->R)) != TG_OK) return st;
+  if (!a->x || !a->ert || !a->slot_alive || !a->w13 || !a->w2 || !a->out)
+    return fail(TG_ERR_NULL_ARG, "a required pointer is NULL");
+  if ((a->w_gate == nullptr) == (a->logits_in == nullptr))
+    return fail(TG_ERR_NULL_ARG, "give exactly one of w_gate and logits_in");
+  return TG_OK;
+}
+
+size_t tg_ew_forward_workspace(const tg_ew_args* a) {
+  if (check_ew(a) != TG_OK) return 0;
+  return ew_layout(a, nullptr).bytes;
+}
+
+static tg_status ew_forward(const tg_ew_args* a, void* ws, size_t ws_bytes, void* stream,
+                            void* const* events) {
+  tg_status st = check_ew(a);
+  if (st != TG_OK) return st;
+  const size_t need = ew_layout(a, nullptr).bytes;
+  if (!ws || ws_bytes < need)
+    return fail(TG_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need, ws_bytes);
+  if (reinterpret_cast<uintptr_t>(ws) & 255)
+    return fail(TG_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  EwLayout L = ew_layout(a, static_cast<char*>(ws));
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  int32_t* ids = a->topk_ids ? a->topk_ids : L.ids;
+  float* w = a->topk_w ? a->topk_w : L.w;
+  int32_t* pair_slot = a->pair_slot ? a->pair_slot : L.pair_slot;
+  int32_t* counts = a->slot_counts ? a->slot_counts : L.counts;
+  int32_t* offsets = a->slot_offsets ? a->slot_offsets : L.offsets;
+  int32_t* pair_row = a->pair_row ? a->pair_row : L.pair_row;
+  int32_t* n_unserved = a->n_unserved ? a->n_unserved : L.n_unserved;
+  const int max_rows = a->T * a->k;
+  hipError_t e = hipSuccess;
+  auto mark = [&](int i) {
+    if (events && e == hipSuccess) e = hipEventRecord(static_cast<hipEvent_t>(events[i]), s);
+  };
+  mark(0);
+  if (e == hipSuccess)
+    e = tg::launch_gate_topk(a->w_gate ? a->x : nullptr, a->w_gate, a->logits_in, a->T, a->d, a->E,
+                             a->k, nullptr, ids, w, s);
+  mark(1);
+  if (e == hipSuccess)
+    e = tg::launch_remap_dispatch(ids, a->T, a->k, a->ert, a->E, a->R, a->slot_alive, a->S, a->x,
+                                  a->d, pair_slot, counts, offsets, L.perm, pair_row, L.x_perm,
+                                  n_unserved, L.dispatch_ws, s);
+  mark(2);
+  if (e == hipSuccess)
+    e = tg::launch_ffn_gateup(L.x_perm, offsets, a->S, max_rows, a->w13, a->d, a->I, L.h, s);
+  mark(3);
+  if (e == hipSuccess)
+    e = tg::launch_ffn_down(L.h, offsets, a->S, max_rows, a->w2, a->d, a->I, L.y, s);
+  mark(4);
+  if (e == hipSuccess) e = tg::launch_combine(L.y, pair_row, w, a->T, a->k, a->d, a->out, s);
+  mark(5);
+  return hip_status(e, "tg_ew_forward");
+}
+
+tg_status tg_ew_forward(const tg_ew_args* a, void* ws, size_t ws_bytes, void* stream) {
+  return ew_forward(a, ws, ws_bytes, stream, nullptr);
+}
+
+tg_status tg_ew_forward_timed(const tg_ew_args* a, void* ws, size_t ws_bytes, void* stream,
+                              void* const* events, int n_events) {
+  if (!events) return fail(TG_ERR_NULL_ARG, "events is NULL");
+  if (n_events != 6) return fail(TG_ERR_BAD_DIM, "n_events=%d, 6 required", n_events);
+  for (int i = 0; i < 6; ++i)
+    if (!events[i]) return fail(TG_ERR_NULL_ARG, "events[%d] is NULL", i);
+  return ew_forward(a, ws, ws_bytes, stream, events);
+}
+
+}  // extern "C"

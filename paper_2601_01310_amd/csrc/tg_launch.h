@@ -1,0 +1,36 @@
+// Internal launchers of the libtg kernels. Arguments are validated by the
+// C-ABI layer (tg_api.cpp) before any of these is called.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace tg {
+
+hipError_t launch_gate_topk(const uint16_t* x, const uint16_t* wg, const float* logits_in, int T,
+                            int d, int E, int k, float* logits_out, int32_t* ids, float* w,
+                            hipStream_t stream);
+
+// Pairs are processed in chunks of kDispatchChunk; the workspace holds one
+// S-wide histogram per chunk and one unserved count per chunk.
+constexpr int kDispatchChunk = 4096;
+size_t dispatch_workspace_bytes(int T, int k, int S);
+hipError_t launch_remap_dispatch(const int32_t* ids, int T, int k, const int32_t* ert, int E, int R,
+                                 const uint8_t* alive, int S, const uint16_t* x, int d,
+                                 int32_t* pair_slot, int32_t* counts, int32_t* offsets,
+                                 int32_t* perm, int32_t* pair_row, uint16_t* x_perm,
+                                 int32_t* n_unserved, void* ws, hipStream_t stream);
+
+hipError_t launch_ffn_gateup(const uint16_t* x_perm, const int32_t* offsets, int S, int max_rows,
+                             const uint16_t* w13, int d, int I, uint16_t* h, hipStream_t stream);
+hipError_t launch_ffn_down(const uint16_t* h, const int32_t* offsets, int S, int max_rows,
+                           const uint16_t* w2, int d, int I, uint16_t* y, hipStream_t stream);
+hipError_t launch_expert_ffn(const uint16_t* x_perm, const int32_t* offsets, int S, int max_rows,
+                             const uint16_t* w13, const uint16_t* w2, int d, int I, uint16_t* h,
+                             uint16_t* y, hipStream_t stream);
+
+hipError_t launch_combine(const uint16_t* y, const int32_t* pair_row, const float* w, int T, int k,
+                          int d, uint16_t* out, hipStream_t stream);
+
+}  // namespace tg

@@ -1,0 +1,146 @@
+"""The C ABI loads, exports every symbol its header declares, and rejects bad
+arguments on the host before anything reaches the GPU (CPU-only tests)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2601_01310_amd import tg
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "tg.h")
+
+# Bogus but non-NULL addresses: every call below fails validation, so none is
+# ever dereferenced or handed to the HIP runtime.
+P = 0x1000
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(tg._LIB_PATH):
+        from paper_2601_01310_amd import build
+        build.build()
+    return tg.load()
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(tg_[a-z_]+)\s*\(", src)))
+
+
+def test_header_declares_the_documented_entry_points():
+    names = declared_functions()
+    assert set(names) == set(tg.EXPORTS), names
+
+
+def test_library_exports_every_declared_symbol(lib):
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def test_status_strings(lib):
+    assert lib.tg_status_string(0) == b"TG_OK"
+    assert lib.tg_status_string(4) == b"TG_ERR_WORKSPACE"
+    assert lib.tg_status_string(99) == b"TG_ERR_UNKNOWN"
+
+
+def _gate(lib, **kw):
+    a = dict(x=P, w_gate=P, logits_in=None, T=4, d=256, E=8, k=2, logits_out=None, ids=P, w=P)
+    a.update(kw)
+    return lib.tg_gate_topk(a["x"], a["w_gate"], a["logits_in"], a["T"], a["d"], a["E"], a["k"],
+                            a["logits_out"], a["ids"], a["w"], None)
+
+
+def test_gate_topk_rejects_bad_arguments(lib):
+    assert _gate(lib, k=9) == tg.TG_ERR_BAD_DIM            # k > E
+    assert _gate(lib, k=0) == tg.TG_ERR_BAD_DIM
+    assert _gate(lib, T=-1) == tg.TG_ERR_BAD_DIM
+    assert _gate(lib, E=2000, k=2) == tg.TG_ERR_UNSUPPORTED
+    assert _gate(lib, E=64, k=33) == tg.TG_ERR_UNSUPPORTED
+    assert _gate(lib, d=200) == tg.TG_ERR_UNSUPPORTED
+    assert _gate(lib, ids=None) == tg.TG_ERR_NULL_ARG
+    assert _gate(lib, w_gate=None) == tg.TG_ERR_NULL_ARG    # x without w_gate
+    assert _gate(lib, logits_in=P) == tg.TG_ERR_NULL_ARG    # both modes at once
+    assert _gate(lib, x=None, w_gate=None) == tg.TG_ERR_NULL_ARG
+    assert b"k=9" in (_gate(lib, k=9) and lib.tg_last_error())
+
+
+def _dispatch(lib, **kw):
+    a = dict(ids=P, T=16, k=2, ert=P, E=8, R=2, alive=P, S=10, x=P, d=256, ps=P, cnt=P, off=P,
+             perm=P, pr=P, xp=P, nu=P, ws=P, wsb=1 << 20)
+    a.update(kw)
+    return lib.tg_remap_dispatch(a["ids"], a["T"], a["k"], a["ert"], a["E"], a["R"], a["alive"],
+                                 a["S"], a["x"], a["d"], a["ps"], a["cnt"], a["off"], a["perm"],
+                                 a["pr"], a["xp"], a["nu"], a["ws"], a["wsb"], None)
+
+
+def test_remap_dispatch_rejects_bad_arguments(lib):
+    need = lib.tg_remap_dispatch_workspace(16, 2, 10)
+    assert need > 0
+    assert _dispatch(lib, wsb=need - 1) == tg.TG_ERR_WORKSPACE
+    assert _dispatch(lib, ws=None) == tg.TG_ERR_WORKSPACE
+    assert _dispatch(lib, ws=P + 8) == tg.TG_ERR_WORKSPACE  # misaligned
+    assert _dispatch(lib, S=0) == tg.TG_ERR_BAD_DIM
+    assert _dispatch(lib, S=1025) == tg.TG_ERR_UNSUPPORTED
+    assert _dispatch(lib, R=17) == tg.TG_ERR_UNSUPPORTED
+    assert _dispatch(lib, perm=None) == tg.TG_ERR_NULL_ARG
+    assert _dispatch(lib, x=None) == tg.TG_ERR_NULL_ARG     # x_perm without x
+    assert _dispatch(lib, d=300) == tg.TG_ERR_UNSUPPORTED
+    assert lib.tg_remap_dispatch_workspace(-1, 2, 10) == 0
+
+
+def test_workspace_grows_with_pairs(lib):
+    small = lib.tg_remap_dispatch_workspace(64, 2, 10)
+    big = lib.tg_remap_dispatch_workspace(1 << 20, 8, 40)
+    assert big > small > 0
+
+
+def _ffn(lib, **kw):
+    a = dict(xp=P, off=P, S=10, rows=128, w13=P, w2=P, d=256, I=512, h=P, y=P)
+    a.update(kw)
+    return lib.tg_expert_ffn_grouped(a["xp"], a["off"], a["S"], a["rows"], a["w13"], a["w2"],
+                                     a["d"], a["I"], a["h"], a["y"], None)
+
+
+def test_expert_ffn_rejects_bad_arguments(lib):
+    assert _ffn(lib, I=100) == tg.TG_ERR_UNSUPPORTED
+    assert _ffn(lib, I=0) == tg.TG_ERR_BAD_DIM
+    assert _ffn(lib, d=128) == tg.TG_ERR_UNSUPPORTED
+    assert _ffn(lib, rows=-1) == tg.TG_ERR_BAD_DIM
+    assert _ffn(lib, S=0) == tg.TG_ERR_BAD_DIM
+    assert _ffn(lib, h=None) == tg.TG_ERR_NULL_ARG
+
+
+def test_combine_rejects_bad_arguments(lib):
+    assert lib.tg_combine(P, P, P, 4, 0, 256, P, None) == tg.TG_ERR_BAD_DIM
+    assert lib.tg_combine(P, P, P, 4, 40, 256, P, None) == tg.TG_ERR_UNSUPPORTED
+    assert lib.tg_combine(P, P, P, 4, 2, 100, P, None) == tg.TG_ERR_UNSUPPORTED
+    assert lib.tg_combine(None, P, P, 4, 2, 256, P, None) == tg.TG_ERR_NULL_ARG
+
+
+def test_ew_forward_rejects_bad_arguments(lib):
+    a = tg.EwArgs()
+    a.T, a.d, a.E, a.k, a.I, a.S, a.R = 8, 256, 8, 2, 512, 10, 2
+    for n in ("x", "w_gate", "ert", "slot_alive", "w13", "w2", "out"):
+        setattr(a, n, P)
+    need = lib.tg_ew_forward_workspace(ctypes.byref(a))
+    assert need > 0
+    assert lib.tg_ew_forward(ctypes.byref(a), P, need - 1, None) == tg.TG_ERR_WORKSPACE
+    a.logits_in = P  # both gating inputs
+    assert lib.tg_ew_forward(ctypes.byref(a), P, need, None) == tg.TG_ERR_NULL_ARG
+    assert lib.tg_ew_forward_workspace(ctypes.byref(a)) == 0
+    a.logits_in = None
+    a.out = None
+    assert lib.tg_ew_forward(ctypes.byref(a), P, need, None) == tg.TG_ERR_NULL_ARG
+    a.out = P
+    a.k = 9
+    assert lib.tg_ew_forward(ctypes.byref(a), P, need, None) == tg.TG_ERR_BAD_DIM
+    assert lib.tg_ew_forward(None, P, need, None) == tg.TG_ERR_NULL_ARG
+
+
+def test_binding_refuses_host_tensors(lib):
+    import torch
+    with pytest.raises(ValueError):
+        tg.tg_combine(torch.zeros(4), None, None, 1, 1, 256, None, stream=0)

@@ -1,0 +1,204 @@
+"""Parity of the HIP path (through the C ABI) with the CPU oracle.
+
+Integer results (top-k ids, slots, counts, offsets, permutation, rows) must
+match bit for bit; bf16 results within |gpu - ref| <= 2e-2 + 1e-2 |ref|;
+gate weights within 1e-6. A run with failed primaries rerouted to shadow
+slots must reproduce the no-failure output bit for bit (§5.1, §5.3).
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import moe_ew as O
+from paper_2601_01310_amd import synth, tg
+from tests import _gpu as G
+from tests._util import host, u16
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+
+
+def _oracle_full(wl, alive=None):
+    a = G.np_inputs(wl, alive)
+    return O.ew_forward(**a, w13=u16(wl.w13), w2=u16(wl.w2))
+
+
+@pytest.fixture(scope="module")
+def tiny():
+    print("[gpu] tiny workload", flush=True)
+    return synth.make("tiny", device=DEV)
+
+
+def test_tiny_each_entry_point_matches_oracle(tiny):
+    g = G.run_stepwise(tiny)
+    r = _oracle_full(tiny)
+    assert np.array_equal(g["logits"], r["logits"]), "float32 logits differ"
+    G.assert_routing_equal(g, r)
+    assert np.array_equal(g["x_perm"], r["x_perm"])
+    G.assert_close_bf16(g["h"], r["h"], "h")
+    G.assert_close_bf16(g["y"], r["y"], "y")
+    G.assert_close_bf16(g["out"], r["out"], "out")
+
+
+def test_tiny_fused_matches_stepwise_and_oracle(tiny):
+    f = G.run_fused(tiny)
+    s = G.run_stepwise(tiny)
+    r = _oracle_full(tiny)
+    G.assert_routing_equal(f, r, check_perm=False)
+    assert np.array_equal(f["out"], s["out"]), "fused and stepwise outputs differ"
+    G.assert_close_bf16(f["out"], r["out"], "out")
+
+
+def test_tiny_failure_rerouted_to_shadow_is_bit_identical(tiny):
+    base = G.run_fused(tiny)
+    alive = tiny.alive_after_failure()  # expert 3's primary fails
+    fail = G.run_fused(tiny, alive)
+    r = _oracle_full(tiny, alive)
+    G.assert_routing_equal(fail, r, check_perm=False)
+    assert fail["counts"][3] == 0 and fail["counts"][9] == base["counts"][3]
+    assert np.array_equal(fail["out"], base["out"])
+
+
+def test_combine_entry_point_on_oracle_intermediates(tiny):
+    r = _oracle_full(tiny)
+    P = int(r["offsets"][-1])
+    y = torch.from_numpy(r["y"].view(np.int16)).view(torch.bfloat16).to(DEV)
+    pr = torch.from_numpy(r["pair_row"]).to(DEV)
+    w = torch.from_numpy(r["w"].astype(np.float32)).to(DEV)
+    out = torch.empty((tiny.T, tiny.d), dtype=torch.bfloat16, device=DEV)
+    tg.tg_combine(y, pr, w, tiny.T, tiny.k, tiny.d, out)
+    torch.cuda.synchronize()
+    assert P == y.shape[0]
+    G.assert_close_bf16(u16(out), r["out"], "combine")
+
+
+def test_ffn_entry_point_rows_independent_of_position(tiny):
+    """The same rows placed at different offsets and in different slots with
+    equal weights give identical bits."""
+    d, I = tiny.d, tiny.I
+    rows = tiny.x[:40].contiguous()
+    x_perm = torch.cat([rows[:13], rows, rows[13:]]).contiguous()  # 13 | 40 | 27 rows
+    # slot 0 gets 13 rows, slot 3 gets 40 rows, slot 9 (shadow of expert 3) 27
+    offsets = torch.zeros(tiny.S + 1, dtype=torch.int32)
+    cnt = torch.zeros(tiny.S, dtype=torch.int32)
+    cnt[0], cnt[3], cnt[9] = 13, 40, 27
+    offsets[1:] = torch.cumsum(cnt, 0)
+    offsets = offsets.to(DEV)
+    h = torch.empty((80, I), dtype=torch.bfloat16, device=DEV)
+    y = torch.empty((80, d), dtype=torch.bfloat16, device=DEV)
+    tg.tg_expert_ffn_grouped(x_perm, offsets, tiny.S, 80, tiny.w13, tiny.w2, d, I, h, y)
+    torch.cuda.synchronize()
+    Y = u16(y)
+    assert np.array_equal(Y[13 + 13:13 + 40], Y[53:80]), "slot 3 vs its shadow slot 9"
+    ref = O.expert_ffn(u16(x_perm[13:53]), u16(tiny.w13[3]), u16(tiny.w2[3]))[1]
+    G.assert_close_bf16(Y[13:53], ref, "y slot 3")
+
+
+def test_repeat_calls_are_bit_identical(tiny):
+    a, b = G.run_fused(tiny), G.run_fused(tiny)
+    for key in a:
+        assert np.array_equal(np.asarray(a[key]), np.asarray(b[key])), key
+
+
+# ---------------------------------------------------------------- random shapes and edge cases
+
+RANDOM_CASES = [
+    # T, d, E, k, I, n_local, shadows, gate, seed
+    (1, 256, 8, 2, 128, 8, [0], "weights", 101),
+    (37, 512, 16, 4, 384, 12, [1, 5, 11], "weights", 102),
+    (200, 256, 64, 6, 256, 20, [0, 7], "logits", 103),
+    (513, 256, 8, 1, 128, 8, [], "weights", 104),
+    (300, 768, 256, 8, 128, 32, [3, 4, 30], "logits", 105),
+    (129, 256, 40, 32, 128, 40, [39], "logits", 106),
+    (1000, 256, 4, 4, 128, 4, [2, 2], "weights", 107),   # k = E; two shadows of one expert
+]
+
+
+@pytest.mark.parametrize("case", RANDOM_CASES, ids=[f"T{c[0]}_E{c[2]}_k{c[3]}" for c in RANDOM_CASES])
+def test_random_shapes_match_oracle(case):
+    T, d, E, k, I, n_local, shadows, gate, seed = case
+    print(f"[gpu] random case {case}", flush=True)
+    wl = synth.make_custom(T=T, d=d, E=E, k=k, I=I, n_local=n_local, shadow_experts=shadows,
+                           gate=gate, seed=seed, device=DEV)
+    rng = np.random.default_rng(seed)
+    alive = wl.alive.clone()
+    dead = rng.choice(wl.S, size=wl.S // 4, replace=False)
+    alive[torch.from_numpy(dead).to(DEV)] = 0
+    for al in (wl.alive, alive):
+        g = G.run_stepwise(wl, al)
+        r = _oracle_full(wl, al)
+        if g["logits"] is not None:
+            assert np.array_equal(g["logits"], r["logits"])
+        G.assert_routing_equal(g, r)
+        assert np.array_equal(g["x_perm"], r["x_perm"])
+        G.assert_close_bf16(g["h"], r["h"], "h")
+        G.assert_close_bf16(g["y"], r["y"], "y")
+        G.assert_close_bf16(g["out"], r["out"], "out")
+
+
+def test_empty_batch():
+    wl = synth.make_custom(T=4, d=256, E=8, k=2, I=128, n_local=8, shadow_experts=[],
+                           gate="weights", seed=5, device=DEV)
+    S = wl.S
+    buf = torch.full((64,), 5, dtype=torch.int32, device=DEV)
+    counts, offsets, nu = buf[:S], buf[16:16 + S + 1], buf[40:41]
+    ids = torch.zeros((8, 2), dtype=torch.int32, device=DEV)
+    ws = tg.workspace(tg.tg_remap_dispatch_workspace(0, 2, S), DEV)
+    tg.tg_remap_dispatch(ids, 0, 2, wl.ert, 8, 2, wl.alive, S, wl.x, 256, ids, counts, offsets,
+                         ids, ids, wl.x, nu, ws, ws.numel())
+    out = wl.x.clone()
+    args = tg.make_ew_args(0, 256, 8, 2, 128, S, 2, wl.x, wl.wg, None, wl.ert, wl.alive, wl.w13,
+                           wl.w2, out)
+    wsb = tg.tg_ew_forward_workspace(args)
+    tg.tg_ew_forward(args, tg.workspace(wsb, DEV), wsb)
+    torch.cuda.synchronize()
+    assert host(counts).tolist() == [0] * S and host(offsets).tolist() == [0] * (S + 1)
+    assert int(nu[0]) == 0
+    assert torch.equal(out, wl.x)  # nothing written for T = 0
+
+
+def test_all_slots_dead_gives_zero_output_and_counts_every_pair():
+    wl = synth.make_custom(T=50, d=256, E=8, k=2, I=128, n_local=8, shadow_experts=[1],
+                           gate="weights", seed=6, device=DEV)
+    alive = torch.zeros_like(wl.alive)
+    f = G.run_fused(wl, alive)
+    assert f["n_unserved"] == 100
+    assert (f["pair_row"] == -1).all() and f["offsets"][-1] == 0
+    assert (f["out"] == 0).all()
+
+
+def test_share_with_no_local_experts_routes_nothing():
+    wl = synth.make_custom(T=64, d=256, E=16, k=2, I=128, n_local=4, shadow_experts=[],
+                           gate="logits", seed=7, device=DEV)
+    ert = torch.full_like(wl.ert, -1)  # this EW hosts nothing that is selected
+    ert[:4, 0] = torch.arange(4, dtype=torch.int32, device=DEV)
+    wl.logits[:, :4] = -30.0
+    wl.ert = ert
+    f = G.run_fused(wl)
+    assert f["offsets"][-1] == 0 and f["n_unserved"] == 0 and (f["out"] == 0).all()
+
+
+# ---------------------------------------------------------------- full-size workloads
+
+FULL = ["mixtral", "dsv3_share", "dsv3_skew", "dsv3_decode"]
+
+
+@pytest.mark.parametrize("name", FULL)
+def test_full_size_routing_exact_and_sampled_outputs(name):
+    print(f"[gpu] full-size {name}", flush=True)
+    wl = synth.make(name, device=DEV)
+    alive_f = wl.alive_after_failure() if wl.fail_experts else wl.alive_after_failure(
+        [wl.slot_expert[wl.S - 1]])  # with no scripted failure, fail the last shadowed expert
+    f0 = G.run_fused(wl)
+    f1 = G.run_fused(wl, alive_f)
+    for al, f in ((wl.alive, f0), (alive_f, f1)):
+        r = O.route(**{k: v for k, v in G.np_inputs(wl, al).items()})
+        G.assert_routing_equal(f, r, check_perm=False)
+    assert np.array_equal(f0["out"], f1["out"]), "failure run differs from no-failure run"
+    assert f0["counts"].sum() == f1["counts"].sum()
+    print(f"[gpu] {name}: P={int(f0['offsets'][-1])} routing exact, failure bit-identical",
+          flush=True)
+    r0 = O.route(**G.np_inputs(wl))
+    toks = G.sample_tokens(r0, wl.T, 128 if name == "dsv3_decode" else 12, seed=1)
+    _, _, _, out_ref = G.oracle_sampled_out(wl, wl.alive, toks)
+    G.assert_close_bf16(f0["out"][toks], out_ref, f"{name} sampled out")
