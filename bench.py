@@ -54,7 +54,7 @@ class HipEvents:
             self.hip.hipEventDestroy(ctypes.c_void_p(e))
 
 
-def cpu_baseline(wl, n_tokens: int = 96):
+def cpu_baseline(wl, n_tokens: int = 1024):
     """The CPU oracle, as it stands, on a bounded sample of the workload:
     the full forward of ``n_tokens`` seeded tokens (their routed pairs)."""
     import numpy as np

@@ -25,7 +25,8 @@
  *   - Calls are reentrant; concurrent calls must not share output or
  *     workspace buffers.
  *   - Shape limits: 1 <= k <= min(E, 32), E <= 1024, 1 <= S <= 1024,
- *     1 <= R <= 16, d % 256 == 0, I % 128 == 0, T * k < 2^31. T may be 0.
+ *     1 <= R <= 16, d % 256 == 0, I % 128 == 0, T * k < 2^31, and one
+ *     slot's weights under 2 GiB (4 * I * d < 2^31 bytes). T may be 0.
  *     Other shapes return TG_ERR_UNSUPPORTED.
  */
 #ifndef TG_H_

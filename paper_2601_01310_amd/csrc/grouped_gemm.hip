@@ -4,19 +4,35 @@
 //   GEMM1  h = bf16(silu(x W1^T) * (x W3^T))   (gate and up fused, SwiGLU)
 //   GEMM2  y = bf16(h W2^T)
 // Rows of slot s are rows offsets[s] .. offsets[s+1]-1 of the activation
-// matrix. Both operands are K-contiguous ("TN"): activations [rows, K] and
-// weights [N, K], so every MFMA fragment is one 16-byte LDS read.
+// matrix. Both operands are K-contiguous: activations [rows, K] and weights
+// [N, K], so every MFMA fragment is one 16-byte LDS read.
 //
-// Tiling (gfx950, wave64): a block of 4 waves computes a BM x BNW tile of
-// (rows x weight rows) with BK = 64 K-steps; waves form a 2x2 grid and each
-// issues v_mfma_f32_32x32x16_bf16 on 32x32 sub-blocks. Tiles are staged
-// through LDS with two buffers (the next K-step's global loads are in flight
-// while the current one is multiplied) and an XOR swizzle of the 16-byte
-// chunks so that fragment reads are bank-conflict free. For GEMM1 the
-// weight tile holds BNW/2 gate rows and the matching BNW/2 up rows, so g and
-// u of one output element land in the same lane and register and the
-// SwiGLU epilogue needs no data exchange. Results are staged through LDS and
-// written as 16-byte row segments.
+// Tiling (gfx950, wave64): a block computes a BM x BN tile of (activation
+// rows x weight rows) in BK-deep K stages with WM x WN waves; each wave
+// issues v_mfma_f32_32x32x16_bf16 on 32x32 sub-blocks with the weight
+// fragment as the first operand, so a lane's accumulators hold four
+// consecutive output columns of one row (packed 8-byte epilogue writes).
+//
+// Staging: both tiles go global -> LDS with buffer loads that write LDS
+// directly (no register staging), NS stages deep. Each 16-byte chunk is
+// placed at an XOR-swizzled position within its row so that fragment reads
+// of consecutive rows hit distinct banks; a lane fetches whichever global
+// chunk the swizzle assigns to its LDS position. The K loop has no branches:
+// each stage ends with one block barrier after which the freed buffer is
+// refilled, and the next stage's first fragments are read while the stage's
+// last MFMAs run. Rows past the end of a group read as zeros through the
+// buffer range check and are never stored.
+//
+// For GEMM1 the weight tile holds BN/2 gate rows and the matching BN/2 up
+// rows and every wave owns equal numbers of both, so g and u of one output
+// element land in the same lane and register and the SwiGLU epilogue needs
+// no data exchange. Results are staged through LDS and written as 16-byte
+// row segments.
+//
+// Tile order: the tiles of one launch are enumerated slot by slot, then by
+// weight panel (n), then by row block (m), so consecutive tiles share a
+// weight panel; each of the 8 XCDs (blocks are dealt to XCDs round robin)
+// takes one contiguous range of that order, keeping a panel in one L2.
 //
 // Every output element is one fixed sequence of MFMA accumulations over K
 // in increasing order, independent of the row's position, its tile or the
@@ -28,242 +44,334 @@
 namespace tg {
 namespace {
 
-constexpr int kThreads = 256;
-constexpr int kBK = 64;  // K per stage: 8 chunks of 8 bf16 per row
+constexpr int kXcds = 8;
 
-__device__ __forceinline__ int swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
-
-// Maps the global m-tile index to (slot, first row, valid rows). Wave 0
-// scans ceil(count/BM) over the slots 64 at a time.
-template <int BM>
-__device__ __forceinline__ bool find_tile(const int32_t* __restrict__ offsets, int S, int mt,
-                                          int* sh /*LDS: slot,row0,rows*/) {
-  if (threadIdx.x < kWave) {
-    const int lane = threadIdx.x;
-    int acc = 0;
-    bool found = false;
-    for (int base = 0; base < S && !found; base += kWave) {
-      const int s = base + lane;
-      int cnt = 0, o = 0;
-      if (s < S) {
-        o = offsets[s];
-        cnt = offsets[s + 1] - o;
-      }
-      const int nt = (cnt + BM - 1) / BM;
-      int incl = nt;
-#pragma unroll
-      for (int off = 1; off < kWave; off <<= 1) {
-        const int v = __shfl_up(incl, off);
-        if (lane >= off) incl += v;
-      }
-      const int excl = incl - nt;
-      const bool mine = (mt >= acc + excl) && (mt < acc + incl);
-      const uint64_t b = __ballot(mine);
-      if (b) {
-        found = true;
-        if (mine) {
-          const int local = mt - acc - excl;
-          sh[0] = s;
-          sh[1] = o + local * BM;
-          sh[2] = min(BM, cnt - local * BM);
-        }
-      }
-      acc += __shfl(incl, kWave - 1);
-    }
-    if (lane == 0 && !found) sh[0] = -1;
-  }
-  __syncthreads();
-  return sh[0] >= 0;
+// XOR swizzle of the 16-byte chunks of a staged row (CH chunks per row);
+// fragment reads of 8 or 16 consecutive rows hit distinct banks.
+template <int CH>
+__device__ __forceinline__ int swz(int r) {
+  if (CH == 8) return (r & 7) ^ ((r >> 3) & 1);
+  return ((r >> 1) ^ (r >> 3)) & 3;
 }
 
-template <int BM, int BNW, bool SWIGLU>
-__global__ __launch_bounds__(kThreads) void grouped_gemm_kernel(
-    const uint16_t* __restrict__ A, const int32_t* __restrict__ offsets, int S,
-    const uint16_t* __restrict__ B, int K, int NW, int I, uint16_t* __restrict__ C, int ldc) {
-  constexpr int MB = BM / 64;    // 32-row MFMA blocks per wave (2 wave rows)
-  constexpr int NB = BNW / 64;   // 32-col MFMA blocks per wave (2 wave cols)
-  constexpr int A_CH = BM * 8 / kThreads;   // 16-byte chunks per thread per stage
-  constexpr int B_CH = BNW * 8 / kThreads;
-  constexpr int BN_OUT = SWIGLU ? BNW / 2 : BNW;
-  constexpr int CP = BN_OUT + 8;  // padded LDS pitch of the output tile (elements)
-  static_assert(BM % 64 == 0 && BNW % 64 == 0, "tile");
-  static_assert(!SWIGLU || NB % 2 == 0, "gate/up halves");
-  static_assert(BM * CP <= 2 * (BM + BNW) * kBK, "epilogue fits in the stage buffers");
+#define TG_WAIT_VM(n) \
+  __builtin_amdgcn_s_waitcnt(((n) & 0xF) | (((n) >> 4) << 14) | (0x7 << 4) | (0xF << 8))
 
-  __shared__ __attribute__((aligned(16))) uint16_t smem[2 * (BM + BNW) * kBK];
-  __shared__ int tile[4];
-  if (!find_tile<BM>(offsets, S, blockIdx.x, tile)) return;
-  const int slot = tile[0], row0 = tile[1], rows = tile[2];
-  const int nt = blockIdx.y;
+__device__ __forceinline__ void block_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// One 16-byte global -> LDS transfer per lane; the wave's 64 chunks land at
+// consecutive 16-byte positions starting at the (wave-uniform) `lds` row.
+typedef __attribute__((address_space(3))) uint16_t lds_u16;
+
+__device__ __forceinline__ void load_lds16(__amdgpu_buffer_rsrc_t rsrc, lds_u16* lds, int voffset,
+                                           int soffset) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (__attribute__((address_space(3))) void*)lds, 16,
+                                           voffset, soffset, 0, 0);
+#endif
+}
+
+// Raw buffer resource over [base, base + bytes); loads beyond it return 0.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+
+struct TileInfo {
+  int slot, row0, rows, nt;
+};
+
+// Wave 0 maps this block to a tile: two passes over the slots (64 per
+// iteration) to total the tiles and then locate the block's logical tile.
+// Returns false (uniformly) when the block has no tile.
+template <int BM>
+__device__ __forceinline__ bool map_tile(const int32_t* __restrict__ offsets, int S, int NT,
+                                         int* sh, TileInfo* t) {
+  if (threadIdx.x < kWave) {
+    const int lane = threadIdx.x;
+    int total = 0;
+    for (int base = 0; base < S; base += kWave) {
+      const int s = base + lane;
+      const int cnt = (s < S) ? offsets[s + 1] - offsets[s] : 0;
+      int v = (cnt + BM - 1) / BM;
+#pragma unroll
+      for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off);
+      total += v;
+    }
+    total *= NT;
+    const int R = (total + kXcds - 1) / kXcds * kXcds;
+    const int b = blockIdx.x;
+    int L = -1;
+    if (b < R) {
+      L = (b % kXcds) * (R / kXcds) + b / kXcds;
+      if (L >= total) L = -1;
+    }
+    if (lane == 0) sh[0] = -1;
+    if (L >= 0) {
+      int acc = 0;  // tiles before this group of slots
+      for (int base = 0; base < S; base += kWave) {
+        const int s = base + lane;
+        int o = 0, cnt = 0;
+        if (s < S) {
+          o = offsets[s];
+          cnt = offsets[s + 1] - o;
+        }
+        const int mt = (cnt + BM - 1) / BM;
+        const int nt_tiles = mt * NT;
+        int incl = nt_tiles;
+#pragma unroll
+        for (int off = 1; off < kWave; off <<= 1) {
+          const int v = __shfl_up(incl, off);
+          if (lane >= off) incl += v;
+        }
+        const int excl = incl - nt_tiles;
+        if (L >= acc + excl && L < acc + incl) {
+          const int local = L - acc - excl;
+          const int n = local / mt, m = local - n * mt;
+          sh[0] = s;
+          sh[1] = o + m * BM;
+          sh[2] = min(BM, cnt - m * BM);
+          sh[3] = n;
+        }
+        const int tot = __shfl(incl, kWave - 1);
+        if (L < acc + tot) break;
+        acc += tot;
+      }
+    }
+  }
+  __syncthreads();
+  t->slot = sh[0];
+  t->row0 = sh[1];
+  t->rows = sh[2];
+  t->nt = sh[3];
+  return t->slot >= 0;
+}
+
+
+
+template <int BM, int BN, int BK, int NS, int WM, int WN, bool SWIGLU>
+__global__ __launch_bounds__(64 * WM * WN) void grouped_gemm_kernel(
+    const uint16_t* __restrict__ A, const int32_t* __restrict__ offsets, int S,
+    const uint16_t* __restrict__ B, int K, int NW, int I, uint16_t* __restrict__ C, int ldc,
+    int NT) {
+  constexpr int NWAVE = WM * WN;
+  constexpr int MB = BM / WM / 32;          // 32-row blocks per wave
+  constexpr int NB = BN / WN / 32;          // 32-col blocks per wave
+  constexpr int CH = BK / 8;                // 16-byte chunks per staged row
+  constexpr int RPI = 64 / CH;              // rows per load instruction (64 lanes x 16 B)
+  constexpr int AI = BM / NWAVE / RPI;      // A load instructions per wave per stage
+  constexpr int BI = BN / NWAVE / RPI;      // B load instructions per wave per stage
+  constexpr int LPS = AI + BI;
+  constexpr int STAGE = (BM + BN) * BK;     // elements per stage
+  constexpr int WOUT = SWIGLU ? BN / 2 / WN : BN / WN;  // output columns per wave
+  constexpr int WP = WOUT + 8;
+  static_assert(MB >= 1 && NB >= 1 && AI >= 1 && BI >= 1 && (BK == 32 || BK == 64), "tile");
+  static_assert(!SWIGLU || NB % 2 == 0, "gate/up halves");
+  static_assert((NS - 2) * LPS <= 63, "vmcnt range");
+  static_assert(NWAVE * 32 * WP <= NS * STAGE, "epilogue fits in the stage buffers");
+
+  __shared__ __attribute__((aligned(16))) uint16_t smem[NS * STAGE];
+  __shared__ int sh[4];
+  TileInfo tile;
+  if (!map_tile<BM>(offsets, S, NT, sh, &tile)) return;
+  const int slot = tile.slot, row0 = tile.row0, rows = tile.rows, nt = tile.nt;
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave / WN, wn = wave % WN;
 
-  // Global source rows of this thread's chunks (fixed over K).
-  const uint16_t* a_src[A_CH];
-  int a_dst[A_CH];
+  // Direct-to-LDS staging: load instruction i of this wave fills RPI
+  // consecutive staged rows (1 KB); lane l writes chunk position l % CH of
+  // row l / CH, so it fetches the global chunk that the swizzle puts there.
+  const size_t b_row0 = (size_t)slot * NW + (SWIGLU ? nt * (BN / 2) : nt * BN);
+  // Rows past the group's end read as zeros (their results are never stored).
+  const __amdgpu_buffer_rsrc_t a_rsrc = make_rsrc(A + (size_t)row0 * K, (uint32_t)rows * K * 2);
+  const __amdgpu_buffer_rsrc_t b_rsrc = make_rsrc(
+      B + b_row0 * K, (uint32_t)min((size_t)0x7fffffff, ((size_t)(slot + 1) * NW - b_row0) * K * 2));
+  int a_off[AI], b_off[BI];  // byte offsets
 #pragma unroll
-  for (int i = 0; i < A_CH; ++i) {
-    const int q = tid + kThreads * i;
-    const int r = q >> 3, c = q & 7;
-    const int gr = row0 + min(r, rows - 1);  // tail rows re-read the last valid row
-    a_src[i] = A + (size_t)gr * K + c * 8;
-    a_dst[i] = r * kBK + ((c ^ swz(r)) << 3);
+  for (int i = 0; i < AI; ++i) {
+    const int r = wave * (BM / NWAVE) + i * RPI + lane / CH;
+    const int c = (lane % CH) ^ swz<CH>(r);
+    a_off[i] = (r * K + c * 8) * 2;
   }
-  const uint16_t* Bslot = B + (size_t)slot * NW * K;
-  const uint16_t* b_src[B_CH];
-  int b_dst[B_CH];
 #pragma unroll
-  for (int i = 0; i < B_CH; ++i) {
-    const int q = tid + kThreads * i;
-    const int r = q >> 3, c = q & 7;
-    int wr;
-    if (SWIGLU)
-      wr = (r < BNW / 2) ? nt * (BNW / 2) + r : I + nt * (BNW / 2) + (r - BNW / 2);
-    else
-      wr = nt * BNW + r;
-    b_src[i] = Bslot + (size_t)wr * K + c * 8;
-    b_dst[i] = r * kBK + ((c ^ swz(r)) << 3);
+  for (int i = 0; i < BI; ++i) {
+    const int r = wave * (BN / NWAVE) + i * RPI + lane / CH;
+    const int c = (lane % CH) ^ swz<CH>(r);
+    const int wr = (SWIGLU && r >= BN / 2) ? I - BN / 2 + r : r;  // up rows follow gate rows
+    b_off[i] = (wr * K + c * 8) * 2;
   }
+  const int a_lds = wave * (BM / NWAVE) * BK;
+  const int b_lds = BM * BK + wave * (BN / NWAVE) * BK;
 
-  // Fragment read offsets (elements) for k16 sub-step 0; sub-step kk adds 2*kk chunks.
-  int a_row[MB], b_row[NB];
-#pragma unroll
-  for (int mb = 0; mb < MB; ++mb) a_row[mb] = wm * (BM / 2) + mb * 32 + (lane & 31);
-#pragma unroll
-  for (int nb = 0; nb < NB; ++nb) {
-    if (SWIGLU)
-      b_row[nb] = (nb < NB / 2) ? wn * (BNW / 4) + nb * 32 + (lane & 31)
-                                : BNW / 2 + wn * (BNW / 4) + (nb - NB / 2) * 32 + (lane & 31);
-    else
-      b_row[nb] = wn * (BNW / 2) + nb * 32 + (lane & 31);
-  }
+  lds_u16* const smem3 = (lds_u16*)smem;
+#define TG_ISSUE(k0, buf)                                                          \
+  do {                                                                             \
+    lds_u16* st_ = smem3 + (buf) * STAGE;                                          \
+    _Pragma("unroll") for (int i = 0; i < AI; ++i)                                 \
+        load_lds16(a_rsrc, st_ + a_lds + i * RPI * BK, a_off[i], (k0) * 2);         \
+    _Pragma("unroll") for (int i = 0; i < BI; ++i)                                 \
+        load_lds16(b_rsrc, st_ + b_lds + i * RPI * BK, b_off[i], (k0) * 2);         \
+  } while (0)
+
+  // LDS element offsets of this lane's fragments for k16 sub-step kk.
   const int khalf = lane >> 5;
-
-  f32x16 acc[MB][NB];
+  const int xrow = wm * (BM / WM) + (lane & 31);
+  const int wrow = (SWIGLU ? wn * (BN / 2 / WN) : wn * (BN / WN)) + (lane & 31);
+  int xoff[BK / 16], woff[BK / 16];
 #pragma unroll
-  for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[mb][nb][r] = 0.0f;
-
-  uint4 ra[A_CH], rb[B_CH];
-#define TG_GLOAD(k0)                                                                        \
-  do {                                                                                      \
-    _Pragma("unroll") for (int i = 0; i < A_CH; ++i) ra[i] =                                \
-        *reinterpret_cast<const uint4*>(a_src[i] + (k0));                                   \
-    _Pragma("unroll") for (int i = 0; i < B_CH; ++i) rb[i] =                                \
-        *reinterpret_cast<const uint4*>(b_src[i] + (k0));                                   \
-  } while (0)
-#define TG_SSTORE(buf)                                                                      \
-  do {                                                                                      \
-    _Pragma("unroll") for (int i = 0; i < A_CH; ++i)                                        \
-        *reinterpret_cast<uint4*>(smem + (buf) * (BM * kBK) + a_dst[i]) = ra[i];            \
-    _Pragma("unroll") for (int i = 0; i < B_CH; ++i)                                        \
-        *reinterpret_cast<uint4*>(smem + 2 * BM * kBK + (buf) * (BNW * kBK) + b_dst[i]) =   \
-            rb[i];                                                                          \
-  } while (0)
-
-  const int nk = K / kBK;
-  TG_GLOAD(0);
-  TG_SSTORE(0);
-  __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    const int cur = kt & 1;
-    if (kt + 1 < nk) TG_GLOAD((kt + 1) * kBK);
-    const uint16_t* as = smem + cur * (BM * kBK);
-    const uint16_t* bs = smem + 2 * BM * kBK + cur * (BNW * kBK);
-#pragma unroll
-    for (int kk = 0; kk < kBK / 16; ++kk) {
-      const int ch = 2 * kk + khalf;
-      bf16x8 af[MB], bfr[NB];
-#pragma unroll
-      for (int mb = 0; mb < MB; ++mb)
-        af[mb] = *reinterpret_cast<const bf16x8*>(as + a_row[mb] * kBK +
-                                                  ((ch ^ swz(a_row[mb])) << 3));
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb)
-        bfr[nb] = *reinterpret_cast<const bf16x8*>(bs + b_row[nb] * kBK +
-                                                   ((ch ^ swz(b_row[nb])) << 3));
-#pragma unroll
-      for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb)
-          acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[mb], bfr[nb], acc[mb][nb], 0, 0, 0);
-    }
-    if (kt + 1 < nk) TG_SSTORE(cur ^ 1);
-    __syncthreads();
+  for (int kk = 0; kk < BK / 16; ++kk) {
+    xoff[kk] = xrow * BK + (((2 * kk + khalf) ^ swz<CH>(xrow)) << 3);
+    woff[kk] = BM * BK + wrow * BK + (((2 * kk + khalf) ^ swz<CH>(wrow)) << 3);
   }
-#undef TG_GLOAD
-#undef TG_SSTORE
+  // Weight rows of block nb relative to wrow (gate blocks, then up blocks).
+  auto wblk = [](int nb) constexpr {
+    return SWIGLU ? ((nb < NB / 2) ? nb * 32 : BN / 2 + (nb - NB / 2) * 32) : nb * 32;
+  };
 
-  // Epilogue: accumulators -> bf16 tile in LDS -> 16-byte row segments.
-  // MFMA 32x32 output: lane l, register r holds row 8*(r/4) + 4*(l/32) + r%4,
-  // column l%32 of its block.
-  uint16_t* Cs = smem;
-  const int mrow = 4 * (lane >> 5);
+  f32x16 acc[NB][MB];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[nb][mb][r] = 0.0f;
+
+  const int nk = K / BK;
+  constexpr int KK = BK / 16;          // k16 sub-steps per stage
+  static_assert(KK % 2 == 0, "fragment double buffering alternates within a stage");
+  bf16x8 xf[2][MB], wf[2][NB];
+#define TG_FRAGS(st, kk, dst)                                                          \
+  do {                                                                                 \
+    _Pragma("unroll") for (int mb = 0; mb < MB; ++mb) xf[dst][mb] =                    \
+        *reinterpret_cast<const bf16x8*>((st) + xoff[kk] + mb * 32 * BK);              \
+    _Pragma("unroll") for (int nb = 0; nb < NB; ++nb) wf[dst][nb] =                    \
+        *reinterpret_cast<const bf16x8*>((st) + woff[kk] + wblk(nb) * BK);             \
+  } while (0)
+#define TG_MFMAS(src)                                                                  \
+  do {                                                                                 \
+    _Pragma("unroll") for (int nb = 0; nb < NB; ++nb)                                  \
+        _Pragma("unroll") for (int mb = 0; mb < MB; ++mb) acc[nb][mb] =                \
+            __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[src][nb], xf[src][mb],          \
+                                                    acc[nb][mb], 0, 0, 0);             \
+  } while (0)
+
+  // Prologue: stages 0..NS-1 in flight (indices past the end re-load the last
+  // stage), stage 0 visible, its first fragments loaded.
+#pragma unroll
+  for (int s = 0; s < NS; ++s) TG_ISSUE(min(s, nk - 1) * BK, s);
+  TG_WAIT_VM((NS - 1) * LPS);
+  block_barrier();
+  TG_FRAGS(smem, 0, 0);
+
+  // Branch-free K loop: every iteration waits, synchronises and refills one
+  // buffer, so each sub-step is one straight-line scheduling region.
+  for (int kt = 0; kt < nk; ++kt) {
+    const uint16_t* st = smem + (kt % NS) * STAGE;
+#pragma unroll
+    for (int kk = 0; kk < KK - 1; ++kk) {
+      TG_FRAGS(st, kk + 1, (kk + 1) & 1);
+      TG_MFMAS(kk & 1);
+    }
+    // Last sub-step: once every wave holds its fragments of this stage and
+    // stage kt+1 has landed, this stage's buffer is refilled with stage
+    // kt+NS (past the end: a harmless re-load of the last stage) and the
+    // next stage's first fragments are read while the last MFMAs run.
+    TG_WAIT_VM((NS - 2) * LPS);
+    __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)
+    block_barrier();
+    TG_ISSUE(min(kt + NS, nk - 1) * BK, kt % NS);
+    TG_FRAGS(smem + ((kt + 1) % NS) * STAGE, 0, 0);
+    TG_MFMAS((KK - 1) & 1);
+  }
+  TG_WAIT_VM(0);
+#undef TG_FRAGS
+#undef TG_MFMAS
+#undef TG_ISSUE
+  __syncthreads();
+
+  // Epilogue. acc[nb][mb] register r of lane l holds row mb*32 + l%32 and
+  // column nb*32 + 8*(r/4) + 4*(l/32) + r%4 of the wave's sub-tile. Each wave
+  // stages one 32-row block at a time in its own LDS region (8-byte writes)
+  // and stores it as 16-byte row segments.
+  uint16_t* region = smem + wave * (32 * WP);
+  const int colbase = SWIGLU ? nt * (BN / 2) + wn * WOUT : nt * BN + wn * WOUT;
+  constexpr int CPR = WOUT / 8;  // 16-byte chunks per wave row
 #pragma unroll
   for (int mb = 0; mb < MB; ++mb) {
-    if (SWIGLU) {
+    const int mm = lane & 31;
 #pragma unroll
-      for (int nb = 0; nb < NB / 2; ++nb) {
-        const int col = wn * (BNW / 4) + nb * 32 + (lane & 31);
+    for (int nb = 0; nb < (SWIGLU ? NB / 2 : NB); ++nb) {
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const float g = acc[mb][nb][r];
-          const float u = acc[mb][nb + NB / 2][r];
-          const float hv = g / (1.0f + __expf(-g)) * u;
-          const int m = wm * (BM / 2) + mb * 32 + 8 * (r >> 2) + mrow + (r & 3);
-          Cs[m * CP + col] = f32_to_bf16(hv);
+      for (int q = 0; q < 4; ++q) {
+        float v[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int r = 4 * q + e;
+          if (SWIGLU) {
+            const float g = acc[nb][mb][r];
+            const float u = acc[nb + NB / 2][mb][r];
+            v[e] = g / (1.0f + __expf(-g)) * u;
+          } else {
+            v[e] = acc[nb][mb][r];
+          }
         }
-      }
-    } else {
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb) {
-        const int col = wn * (BNW / 2) + nb * 32 + (lane & 31);
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int m = wm * (BM / 2) + mb * 32 + 8 * (r >> 2) + mrow + (r & 3);
-          Cs[m * CP + col] = f32_to_bf16(acc[mb][nb][r]);
-        }
+        const int col = nb * 32 + 8 * q + 4 * (lane >> 5);
+        uint2 pk;
+        pk.x = pack_bf16x2(v[0], v[1]);
+        pk.y = pack_bf16x2(v[2], v[3]);
+        *reinterpret_cast<uint2*>(region + mm * WP + col) = pk;
       }
     }
-  }
-  __syncthreads();
-  constexpr int CPR = BN_OUT / 8;  // 16-byte chunks per output row
-  for (int q = tid; q < BM * CPR; q += kThreads) {
-    const int r = q / CPR, c = q - r * CPR;
-    if (r < rows) {
-      *reinterpret_cast<uint4*>(C + (size_t)(row0 + r) * ldc + nt * BN_OUT + c * 8) =
-          *reinterpret_cast<const uint4*>(Cs + r * CP + c * 8);
+    __syncthreads();
+    const int mbase = wm * (BM / WM) + mb * 32;
+#pragma unroll
+    for (int i = 0; i < (32 * CPR + kWave - 1) / kWave; ++i) {
+      const int q = lane + kWave * i;
+      const int r = q / CPR, c = q - r * CPR;
+      if (q < 32 * CPR && mbase + r < rows) {
+        *reinterpret_cast<uint4*>(C + (size_t)(row0 + mbase + r) * ldc + colbase + c * 8) =
+            *reinterpret_cast<const uint4*>(region + r * WP + c * 8);
+      }
     }
+    __syncthreads();
   }
 }
 
-constexpr int kBM = 128;
-constexpr int kBNW = 256;
+template <int BM, int BN, int BK, int NS, int WM, int WN, bool SWIGLU>
+hipError_t launch_grouped(const uint16_t* A, const int32_t* offsets, int S, int max_rows,
+                          const uint16_t* B, int K, int NW, int I, uint16_t* C, int ldc, int NT,
+                          hipStream_t stream) {
+  // Bound on the tile count: sum_s ceil(count_s / BM) <= ceil(max_rows / BM) + S.
+  const long bound = ((long)(max_rows + BM - 1) / BM + S) * NT;
+  const long grid = (bound + kXcds - 1) / kXcds * kXcds;
+  hipLaunchKernelGGL((grouped_gemm_kernel<BM, BN, BK, NS, WM, WN, SWIGLU>), dim3((unsigned)grid),
+                     dim3(64 * WM * WN), 0, stream, A, offsets, S, B, K, NW, I, C, ldc, NT);
+  return hipGetLastError();
+}
+
+// 256 x 256 tiles, 64-deep double-buffered stages, 16 waves (4 per SIMD).
+constexpr int kBM = 256, kBN = 256, kBK = 64, kNS = 2, kWM = 4, kWN = 4;
 
 }  // namespace
 
 hipError_t launch_ffn_gateup(const uint16_t* x_perm, const int32_t* offsets, int S, int max_rows,
                              const uint16_t* w13, int d, int I, uint16_t* h, hipStream_t stream) {
   if (max_rows == 0) return hipSuccess;
-  const int mtiles = (max_rows + kBM - 1) / kBM + S;  // bound on sum_s ceil(count_s / BM)
-  hipLaunchKernelGGL((grouped_gemm_kernel<kBM, kBNW, true>), dim3(mtiles, (2 * I) / kBNW),
-                     dim3(kThreads), 0, stream, x_perm, offsets, S, w13, d, 2 * I, I, h, I);
-  return hipGetLastError();
+  return launch_grouped<kBM, kBN, kBK, kNS, kWM, kWN, true>(
+      x_perm, offsets, S, max_rows, w13, d, 2 * I, I, h, I, (2 * I) / kBN, stream);
 }
 
 hipError_t launch_ffn_down(const uint16_t* h, const int32_t* offsets, int S, int max_rows,
                            const uint16_t* w2, int d, int I, uint16_t* y, hipStream_t stream) {
   if (max_rows == 0) return hipSuccess;
-  const int mtiles = (max_rows + kBM - 1) / kBM + S;
-  hipLaunchKernelGGL((grouped_gemm_kernel<kBM, kBNW, false>), dim3(mtiles, d / kBNW),
-                     dim3(kThreads), 0, stream, h, offsets, S, w2, I, d, 0, y, d);
-  return hipGetLastError();
+  return launch_grouped<kBM, kBN, kBK, kNS, kWM, kWN, false>(
+      h, offsets, S, max_rows, w2, I, d, 0, y, d, d / kBN, stream);
 }
 
 hipError_t launch_expert_ffn(const uint16_t* x_perm, const int32_t* offsets, int S, int max_rows,

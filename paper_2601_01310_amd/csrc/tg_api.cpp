@@ -57,6 +57,17 @@ tg_status check_inter(int I) {
   return TG_OK;
 }
 
+// One slot's gate/up weights are addressed with 32-bit byte offsets.
+tg_status check_ffn(int d, int I) {
+  tg_status st = check_hidden(d, "d");
+  if (st != TG_OK) return st;
+  if ((st = check_inter(I)) != TG_OK) return st;
+  if (4LL * I * d >= (1LL << 31))
+    return fail(TG_ERR_UNSUPPORTED, "one slot's weights (4*I*d = %lld bytes) reach 2 GiB",
+                4LL * I * d);
+  return TG_OK;
+}
+
 tg_status check_slots(int S, int R) {
   if (S <= 0 || R <= 0) return fail(TG_ERR_BAD_DIM, "S=%d and R=%d must be > 0", S, R);
   if (S > kMaxS) return fail(TG_ERR_UNSUPPORTED, "S=%d exceeds %d", S, kMaxS);
@@ -184,8 +195,7 @@ tg_status tg_expert_ffn_grouped(const uint16_t* x_perm, const int32_t* slot_offs
   if (S <= 0) return fail(TG_ERR_BAD_DIM, "S=%d must be > 0", S);
   if (S > kMaxS) return fail(TG_ERR_UNSUPPORTED, "S=%d exceeds %d", S, kMaxS);
   if (max_rows < 0) return fail(TG_ERR_BAD_DIM, "max_rows=%d must be >= 0", max_rows);
-  if ((st = check_hidden(d, "d")) != TG_OK) return st;
-  if ((st = check_inter(I)) != TG_OK) return st;
+  if ((st = check_ffn(d, I)) != TG_OK) return st;
   if (!x_perm || !slot_offsets || !w13 || !w2 || !h || !y)
     return fail(TG_ERR_NULL_ARG, "a required pointer is NULL");
   return hip_status(tg::launch_expert_ffn(x_perm, slot_offsets, S, max_rows, w13, w2, d, I, h, y,
@@ -209,8 +219,7 @@ static tg_status check_ew(const tg_ew_args* a) {
   if (!a) return fail(TG_ERR_NULL_ARG, "args is NULL");
   tg_status st = check_gate_dims(a->T, a->E, a->k);
   if (st != TG_OK) return st;
-  if ((st = check_hidden(a->d, "d")) != TG_OK) return st;
-  if ((st = check_inter(a->I)) != TG_OK) return st;
+  if ((st = check_ffn(a->d, a->I)) != TG_OK) return st;
   if ((st = check_slots(a->S, a->R)) != TG_OK) return st;
   if (!a->x || !a->ert || !a->slot_alive || !a->w13 || !a->w2 || !a->out)
     return fail(TG_ERR_NULL_ARG, "a required pointer is NULL");

@@ -111,6 +111,7 @@ def test_expert_ffn_rejects_bad_arguments(lib):
     assert _ffn(lib, rows=-1) == tg.TG_ERR_BAD_DIM
     assert _ffn(lib, S=0) == tg.TG_ERR_BAD_DIM
     assert _ffn(lib, h=None) == tg.TG_ERR_NULL_ARG
+    assert _ffn(lib, d=16384, I=32768) == tg.TG_ERR_UNSUPPORTED  # 2 GiB per slot
 
 
 def test_combine_rejects_bad_arguments(lib):
