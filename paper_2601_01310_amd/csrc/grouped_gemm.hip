@@ -14,20 +14,23 @@
 // consecutive output columns of one row (packed 8-byte epilogue writes).
 //
 // Staging: both tiles go global -> LDS with buffer loads that write LDS
-// directly (no register staging), NS stages deep. Each 16-byte chunk is
-// placed at an XOR-swizzled position within its row so that fragment reads
-// of consecutive rows hit distinct banks; a lane fetches whichever global
-// chunk the swizzle assigns to its LDS position. The K loop has no branches:
-// each stage ends with one block barrier after which the freed buffer is
-// refilled, and the next stage's first fragments are read while the stage's
-// last MFMAs run. Rows past the end of a group read as zeros through the
-// buffer range check and are never stored.
+// directly (no register staging). Activation stages are double-buffered and
+// weight stages triple-buffered (weights are first touched in HBM, so they
+// are requested two stages ahead); at 256 x 256 x 64 this fills the 160 KB
+// of LDS. Each 16-byte chunk sits at an XOR-swizzled position within its
+// row so that fragment reads of consecutive rows hit distinct banks; a lane
+// fetches whichever global chunk the swizzle assigns to its LDS position.
+// The K loop has no branches: each stage ends with one block barrier after
+// which the freed buffers are refilled, and the next stage's first
+// fragments are read while the stage's last MFMAs run. Rows past the end of
+// a group read as zeros through the buffer range check and are never
+// stored; waves whose rows all lie past the end skip their MFMAs.
 //
 // For GEMM1 the weight tile holds BN/2 gate rows and the matching BN/2 up
 // rows and every wave owns equal numbers of both, so g and u of one output
 // element land in the same lane and register and the SwiGLU epilogue needs
-// no data exchange. Results are staged through LDS and written as 16-byte
-// row segments.
+// no data exchange. Results are staged through each wave's own LDS region
+// and written as 16-byte row segments.
 //
 // Tile order: the tiles of one launch are enumerated slot by slot, then by
 // weight panel (n), then by row block (m), so consecutive tiles share a
@@ -63,10 +66,10 @@ __device__ __forceinline__ void block_barrier() {
   asm volatile("" ::: "memory");
 }
 
-// One 16-byte global -> LDS transfer per lane; the wave's 64 chunks land at
-// consecutive 16-byte positions starting at the (wave-uniform) `lds` row.
 typedef __attribute__((address_space(3))) uint16_t lds_u16;
 
+// One 16-byte global -> LDS transfer per lane; the wave's 64 chunks land at
+// consecutive 16-byte positions starting at the (wave-uniform) `lds` row.
 __device__ __forceinline__ void load_lds16(__amdgpu_buffer_rsrc_t rsrc, lds_u16* lds, int voffset,
                                            int soffset) {
 #if defined(__HIP_DEVICE_COMPILE__)
@@ -84,75 +87,66 @@ struct TileInfo {
   int slot, row0, rows, nt;
 };
 
-// Wave 0 maps this block to a tile: two passes over the slots (64 per
-// iteration) to total the tiles and then locate the block's logical tile.
-// Returns false (uniformly) when the block has no tile.
+// Every wave maps the block to its tile on its own (no LDS, no barrier): two
+// passes over the slots, 64 per iteration, to total the tiles and then find
+// the block's logical tile. Returns false (uniformly) when there is none.
 template <int BM>
 __device__ __forceinline__ bool map_tile(const int32_t* __restrict__ offsets, int S, int NT,
-                                         int* sh, TileInfo* t) {
-  if (threadIdx.x < kWave) {
-    const int lane = threadIdx.x;
-    int total = 0;
-    for (int base = 0; base < S; base += kWave) {
-      const int s = base + lane;
-      const int cnt = (s < S) ? offsets[s + 1] - offsets[s] : 0;
-      int v = (cnt + BM - 1) / BM;
+                                         TileInfo* t) {
+  const int lane = threadIdx.x & 63;
+  int total = 0;
+  for (int base = 0; base < S; base += kWave) {
+    const int s = base + lane;
+    const int cnt = (s < S) ? offsets[s + 1] - offsets[s] : 0;
+    int v = (cnt + BM - 1) / BM;
 #pragma unroll
-      for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off);
-      total += v;
-    }
-    total *= NT;
-    const int R = (total + kXcds - 1) / kXcds * kXcds;
-    const int b = blockIdx.x;
-    int L = -1;
-    if (b < R) {
-      L = (b % kXcds) * (R / kXcds) + b / kXcds;
-      if (L >= total) L = -1;
-    }
-    if (lane == 0) sh[0] = -1;
-    if (L >= 0) {
-      int acc = 0;  // tiles before this group of slots
-      for (int base = 0; base < S; base += kWave) {
-        const int s = base + lane;
-        int o = 0, cnt = 0;
-        if (s < S) {
-          o = offsets[s];
-          cnt = offsets[s + 1] - o;
-        }
-        const int mt = (cnt + BM - 1) / BM;
-        const int nt_tiles = mt * NT;
-        int incl = nt_tiles;
-#pragma unroll
-        for (int off = 1; off < kWave; off <<= 1) {
-          const int v = __shfl_up(incl, off);
-          if (lane >= off) incl += v;
-        }
-        const int excl = incl - nt_tiles;
-        if (L >= acc + excl && L < acc + incl) {
-          const int local = L - acc - excl;
-          const int n = local / mt, m = local - n * mt;
-          sh[0] = s;
-          sh[1] = o + m * BM;
-          sh[2] = min(BM, cnt - m * BM);
-          sh[3] = n;
-        }
-        const int tot = __shfl(incl, kWave - 1);
-        if (L < acc + tot) break;
-        acc += tot;
-      }
-    }
+    for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off);
+    total += v;
   }
-  __syncthreads();
-  t->slot = sh[0];
-  t->row0 = sh[1];
-  t->rows = sh[2];
-  t->nt = sh[3];
-  return t->slot >= 0;
+  total = __builtin_amdgcn_readfirstlane(total) * NT;
+  const int R = (total + kXcds - 1) / kXcds * kXcds;
+  const int b = blockIdx.x;
+  if (b >= R) return false;
+  const int L = (b % kXcds) * (R / kXcds) + b / kXcds;
+  if (L >= total) return false;
+  int acc = 0;  // tiles before this group of slots
+  for (int base = 0; base < S; base += kWave) {
+    const int s = base + lane;
+    int o = 0, cnt = 0;
+    if (s < S) {
+      o = offsets[s];
+      cnt = offsets[s + 1] - o;
+    }
+    const int mt = (cnt + BM - 1) / BM;
+    const int tiles = mt * NT;
+    int incl = tiles;
+#pragma unroll
+    for (int off = 1; off < kWave; off <<= 1) {
+      const int v = __shfl_up(incl, off);
+      if (lane >= off) incl += v;
+    }
+    const int excl = incl - tiles;
+    const uint64_t owner = __ballot(L >= acc + excl && L < acc + incl);
+    if (owner) {
+      const int src = __builtin_ctzll(owner);
+      const int local = L - acc - __shfl(excl, src);
+      const int m_t = __shfl(mt, src);
+      const int n = local / m_t, m = local - n * m_t;
+      t->slot = __builtin_amdgcn_readfirstlane(base + src);
+      t->row0 = __builtin_amdgcn_readfirstlane(__shfl(o, src) + m * BM);
+      t->rows = __builtin_amdgcn_readfirstlane(min(BM, __shfl(cnt, src) - m * BM));
+      t->nt = __builtin_amdgcn_readfirstlane(n);
+      return true;
+    }
+    acc += __shfl(incl, kWave - 1);
+  }
+  return false;
 }
 
-
-
-template <int BM, int BN, int BK, int NS, int WM, int WN, bool SWIGLU>
+// A (activation) tiles are double-buffered and B (weight) tiles triple-
+// buffered: weight slices are first touched in HBM, so they are requested
+// two stages ahead; activation slices are reused from cache.
+template <int BM, int BN, int BK, int WM, int WN, bool SWIGLU>
 __global__ __launch_bounds__(64 * WM * WN) void grouped_gemm_kernel(
     const uint16_t* __restrict__ A, const int32_t* __restrict__ offsets, int S,
     const uint16_t* __restrict__ B, int K, int NW, int I, uint16_t* __restrict__ C, int ldc,
@@ -164,19 +158,16 @@ __global__ __launch_bounds__(64 * WM * WN) void grouped_gemm_kernel(
   constexpr int RPI = 64 / CH;              // rows per load instruction (64 lanes x 16 B)
   constexpr int AI = BM / NWAVE / RPI;      // A load instructions per wave per stage
   constexpr int BI = BN / NWAVE / RPI;      // B load instructions per wave per stage
-  constexpr int LPS = AI + BI;
-  constexpr int STAGE = (BM + BN) * BK;     // elements per stage
+  constexpr int A_ST = BM * BK, B_ST = BN * BK;  // elements per stage buffer
   constexpr int WOUT = SWIGLU ? BN / 2 / WN : BN / WN;  // output columns per wave
   constexpr int WP = WOUT + 8;
   static_assert(MB >= 1 && NB >= 1 && AI >= 1 && BI >= 1 && (BK == 32 || BK == 64), "tile");
   static_assert(!SWIGLU || NB % 2 == 0, "gate/up halves");
-  static_assert((NS - 2) * LPS <= 63, "vmcnt range");
-  static_assert(NWAVE * 32 * WP <= NS * STAGE, "epilogue fits in the stage buffers");
+  static_assert(NWAVE * 32 * WP <= 2 * A_ST + 3 * B_ST, "epilogue fits in the stage buffers");
 
-  __shared__ __attribute__((aligned(16))) uint16_t smem[NS * STAGE];
-  __shared__ int sh[4];
+  __shared__ __attribute__((aligned(16))) uint16_t smem[2 * A_ST + 3 * B_ST];
   TileInfo tile;
-  if (!map_tile<BM>(offsets, S, NT, sh, &tile)) return;
+  if (!map_tile<BM>(offsets, S, NT, &tile)) return;
   const int slot = tile.slot, row0 = tile.row0, rows = tile.rows, nt = tile.nt;
 
   const int tid = threadIdx.x;
@@ -206,17 +197,20 @@ __global__ __launch_bounds__(64 * WM * WN) void grouped_gemm_kernel(
     const int wr = (SWIGLU && r >= BN / 2) ? I - BN / 2 + r : r;  // up rows follow gate rows
     b_off[i] = (wr * K + c * 8) * 2;
   }
-  const int a_lds = wave * (BM / NWAVE) * BK;
-  const int b_lds = BM * BK + wave * (BN / NWAVE) * BK;
-
   lds_u16* const smem3 = (lds_u16*)smem;
-#define TG_ISSUE(k0, buf)                                                          \
+  const int a_lds = wave * (BM / NWAVE) * BK;
+  const int b_lds = 2 * A_ST + wave * (BN / NWAVE) * BK;
+#define TG_ISSUE_A(k0, buf)                                                        \
   do {                                                                             \
-    lds_u16* st_ = smem3 + (buf) * STAGE;                                          \
     _Pragma("unroll") for (int i = 0; i < AI; ++i)                                 \
-        load_lds16(a_rsrc, st_ + a_lds + i * RPI * BK, a_off[i], (k0) * 2);         \
+        load_lds16(a_rsrc, smem3 + (buf) * A_ST + a_lds + i * RPI * BK, a_off[i],   \
+                   (k0) * 2);                                                      \
+  } while (0)
+#define TG_ISSUE_B(k0, buf)                                                        \
+  do {                                                                             \
     _Pragma("unroll") for (int i = 0; i < BI; ++i)                                 \
-        load_lds16(b_rsrc, st_ + b_lds + i * RPI * BK, b_off[i], (k0) * 2);         \
+        load_lds16(b_rsrc, smem3 + (buf) * B_ST + b_lds + i * RPI * BK, b_off[i],   \
+                   (k0) * 2);                                                      \
   } while (0)
 
   // LDS element offsets of this lane's fragments for k16 sub-step kk.
@@ -227,7 +221,7 @@ __global__ __launch_bounds__(64 * WM * WN) void grouped_gemm_kernel(
 #pragma unroll
   for (int kk = 0; kk < BK / 16; ++kk) {
     xoff[kk] = xrow * BK + (((2 * kk + khalf) ^ swz<CH>(xrow)) << 3);
-    woff[kk] = BM * BK + wrow * BK + (((2 * kk + khalf) ^ swz<CH>(wrow)) << 3);
+    woff[kk] = 2 * A_ST + wrow * BK + (((2 * kk + khalf) ^ swz<CH>(wrow)) << 3);
   }
   // Weight rows of block nb relative to wrow (gate blocks, then up blocks).
   auto wblk = [](int nb) constexpr {
@@ -246,12 +240,14 @@ __global__ __launch_bounds__(64 * WM * WN) void grouped_gemm_kernel(
   constexpr int KK = BK / 16;          // k16 sub-steps per stage
   static_assert(KK % 2 == 0, "fragment double buffering alternates within a stage");
   bf16x8 xf[2][MB], wf[2][NB];
-#define TG_FRAGS(st, kk, dst)                                                          \
+#define TG_FRAGS(abuf, bbuf, kk, dst)                                                  \
   do {                                                                                 \
     _Pragma("unroll") for (int mb = 0; mb < MB; ++mb) xf[dst][mb] =                    \
-        *reinterpret_cast<const bf16x8*>((st) + xoff[kk] + mb * 32 * BK);              \
+        *reinterpret_cast<const bf16x8*>(smem + (abuf) * A_ST + xoff[kk] +             \
+                                         mb * 32 * BK);                                \
     _Pragma("unroll") for (int nb = 0; nb < NB; ++nb) wf[dst][nb] =                    \
-        *reinterpret_cast<const bf16x8*>((st) + woff[kk] + wblk(nb) * BK);             \
+        *reinterpret_cast<const bf16x8*>(smem + (bbuf) * B_ST + woff[kk] +             \
+                                         wblk(nb) * BK);                               \
   } while (0)
 #define TG_MFMAS(src)                                                                  \
   do {                                                                                 \
@@ -261,38 +257,55 @@ __global__ __launch_bounds__(64 * WM * WN) void grouped_gemm_kernel(
                                                     acc[nb][mb], 0, 0, 0);             \
   } while (0)
 
-  // Prologue: stages 0..NS-1 in flight (indices past the end re-load the last
-  // stage), stage 0 visible, its first fragments loaded.
-#pragma unroll
-  for (int s = 0; s < NS; ++s) TG_ISSUE(min(s, nk - 1) * BK, s);
-  TG_WAIT_VM((NS - 1) * LPS);
+  // Prologue: A stages 0-1 and B stages 0-2 in flight (indices past the end
+  // re-load the last stage); stage 0 visible; its first fragments loaded.
+  TG_ISSUE_A(0, 0);
+  TG_ISSUE_B(0, 0);
+  TG_ISSUE_B(min(1, nk - 1) * BK, 1);
+  TG_ISSUE_A(min(1, nk - 1) * BK, 1);
+  TG_ISSUE_B(min(2, nk - 1) * BK, 2);
+  TG_WAIT_VM(2 * BI + AI);
   block_barrier();
-  TG_FRAGS(smem, 0, 0);
+  TG_FRAGS(0, 0, 0, 0);
 
   // Branch-free K loop: every iteration waits, synchronises and refills one
-  // buffer, so each sub-step is one straight-line scheduling region.
-  for (int kt = 0; kt < nk; ++kt) {
-    const uint16_t* st = smem + (kt % NS) * STAGE;
+  // A buffer and one B buffer, so each sub-step is one straight-line region.
+  // A wave whose rows all lie past the group's end (in the tail tile of a
+  // slot) skips the fragment reads and MFMAs but keeps its loads and
+  // barriers.
+  if (wm * (BM / WM) < rows) {
+    for (int kt = 0; kt < nk; ++kt) {
+      const int ab = kt & 1, bb = kt % 3;
 #pragma unroll
-    for (int kk = 0; kk < KK - 1; ++kk) {
-      TG_FRAGS(st, kk + 1, (kk + 1) & 1);
-      TG_MFMAS(kk & 1);
+      for (int kk = 0; kk < KK - 1; ++kk) {
+        TG_FRAGS(ab, bb, kk + 1, (kk + 1) & 1);
+        TG_MFMAS(kk & 1);
+      }
+      // Last sub-step: once every wave holds its fragments of stage kt and
+      // stage kt+1 has landed (only B of stage kt+2 may still be in flight),
+      // stage kt's buffers take A of stage kt+2 and B of stage kt+3, and the
+      // next stage's first fragments are read while the last MFMAs run.
+      TG_WAIT_VM(BI);
+      __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)
+      block_barrier();
+      TG_ISSUE_A(min(kt + 2, nk - 1) * BK, ab);
+      TG_ISSUE_B(min(kt + 3, nk - 1) * BK, bb);
+      TG_FRAGS((kt + 1) & 1, (kt + 1) % 3, 0, 0);
+      TG_MFMAS((KK - 1) & 1);
     }
-    // Last sub-step: once every wave holds its fragments of this stage and
-    // stage kt+1 has landed, this stage's buffer is refilled with stage
-    // kt+NS (past the end: a harmless re-load of the last stage) and the
-    // next stage's first fragments are read while the last MFMAs run.
-    TG_WAIT_VM((NS - 2) * LPS);
-    __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)
-    block_barrier();
-    TG_ISSUE(min(kt + NS, nk - 1) * BK, kt % NS);
-    TG_FRAGS(smem + ((kt + 1) % NS) * STAGE, 0, 0);
-    TG_MFMAS((KK - 1) & 1);
+  } else {
+    for (int kt = 0; kt < nk; ++kt) {
+      TG_WAIT_VM(BI);
+      block_barrier();
+      TG_ISSUE_A(min(kt + 2, nk - 1) * BK, kt & 1);
+      TG_ISSUE_B(min(kt + 3, nk - 1) * BK, kt % 3);
+    }
   }
   TG_WAIT_VM(0);
 #undef TG_FRAGS
 #undef TG_MFMAS
-#undef TG_ISSUE
+#undef TG_ISSUE_A
+#undef TG_ISSUE_B
   __syncthreads();
 
   // Epilogue. acc[nb][mb] register r of lane l holds row mb*32 + l%32 and
@@ -328,7 +341,10 @@ __global__ __launch_bounds__(64 * WM * WN) void grouped_gemm_kernel(
         *reinterpret_cast<uint2*>(region + mm * WP + col) = pk;
       }
     }
-    __syncthreads();
+    // The region is this wave's own: LDS completes a wave's accesses in
+    // order, so only the compiler must keep the reads after the writes.
+    __builtin_amdgcn_s_waitcnt(0xc07f);
+    asm volatile("" ::: "memory");
     const int mbase = wm * (BM / WM) + mb * 32;
 #pragma unroll
     for (int i = 0; i < (32 * CPR + kWave - 1) / kWave; ++i) {
@@ -339,39 +355,39 @@ __global__ __launch_bounds__(64 * WM * WN) void grouped_gemm_kernel(
             *reinterpret_cast<const uint4*>(region + r * WP + c * 8);
       }
     }
-    __syncthreads();
+    __builtin_amdgcn_s_waitcnt(0xc07f);
+    asm volatile("" ::: "memory");
   }
 }
 
-template <int BM, int BN, int BK, int NS, int WM, int WN, bool SWIGLU>
+template <int BM, int BN, int BK, int WM, int WN, bool SWIGLU>
 hipError_t launch_grouped(const uint16_t* A, const int32_t* offsets, int S, int max_rows,
                           const uint16_t* B, int K, int NW, int I, uint16_t* C, int ldc, int NT,
                           hipStream_t stream) {
   // Bound on the tile count: sum_s ceil(count_s / BM) <= ceil(max_rows / BM) + S.
   const long bound = ((long)(max_rows + BM - 1) / BM + S) * NT;
   const long grid = (bound + kXcds - 1) / kXcds * kXcds;
-  hipLaunchKernelGGL((grouped_gemm_kernel<BM, BN, BK, NS, WM, WN, SWIGLU>), dim3((unsigned)grid),
+  hipLaunchKernelGGL((grouped_gemm_kernel<BM, BN, BK, WM, WN, SWIGLU>), dim3((unsigned)grid),
                      dim3(64 * WM * WN), 0, stream, A, offsets, S, B, K, NW, I, C, ldc, NT);
   return hipGetLastError();
 }
 
-// 256 x 256 tiles, 64-deep double-buffered stages, 16 waves (4 per SIMD).
-constexpr int kBM = 256, kBN = 256, kBK = 64, kNS = 2, kWM = 4, kWN = 4;
+constexpr int kBM = 256, kBN = 256, kBK = 64, kWM = 4, kWN = 4;
 
 }  // namespace
 
 hipError_t launch_ffn_gateup(const uint16_t* x_perm, const int32_t* offsets, int S, int max_rows,
                              const uint16_t* w13, int d, int I, uint16_t* h, hipStream_t stream) {
   if (max_rows == 0) return hipSuccess;
-  return launch_grouped<kBM, kBN, kBK, kNS, kWM, kWN, true>(
-      x_perm, offsets, S, max_rows, w13, d, 2 * I, I, h, I, (2 * I) / kBN, stream);
+  return launch_grouped<kBM, kBN, kBK, kWM, kWN, true>(x_perm, offsets, S, max_rows, w13, d,
+                                                       2 * I, I, h, I, (2 * I) / kBN, stream);
 }
 
 hipError_t launch_ffn_down(const uint16_t* h, const int32_t* offsets, int S, int max_rows,
                            const uint16_t* w2, int d, int I, uint16_t* y, hipStream_t stream) {
   if (max_rows == 0) return hipSuccess;
-  return launch_grouped<kBM, kBN, kBK, kNS, kWM, kWN, false>(
-      h, offsets, S, max_rows, w2, I, d, 0, y, d, d / kBN, stream);
+  return launch_grouped<kBM, kBN, kBK, kWM, kWN, false>(h, offsets, S, max_rows, w2, I, d, 0, y,
+                                                        d, d / kBN, stream);
 }
 
 hipError_t launch_expert_ffn(const uint16_t* x_perm, const int32_t* offsets, int S, int max_rows,
