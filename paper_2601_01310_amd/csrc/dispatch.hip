@@ -7,7 +7,7 @@
 //      (integer LDS atomics: the totals do not depend on their order);
 //   2. scan: per-slot totals, exclusive slot offsets, and the base row of
 //      every (chunk, slot) in chunk order;
-//   3. scatter: each wave walks its quarter of a chunk in pair order and
+//   3. scatter: each wave walks an equal share of a chunk in pair order and
 //      ranks equal slots with ballots, so rows follow (slot, token, rank).
 // The gather then copies one activation row per routed pair with 16-byte
 // loads and stores (rows are contiguous in source and destination, so the
@@ -24,14 +24,14 @@ constexpr int kBlock = 256;
 __global__ __launch_bounds__(kBlock) void remap_count_kernel(
     const int32_t* __restrict__ ids, int npairs, const int32_t* __restrict__ ert, int E, int R,
     const uint8_t* __restrict__ alive, int S, int32_t* __restrict__ pair_slot,
-    int32_t* __restrict__ hist, int32_t* __restrict__ unserved_chunk) {
+    int32_t* __restrict__ hist, int32_t* __restrict__ unserved_chunk, int chunk) {
   __shared__ int h[kMaxS];
   __shared__ int nu;
   for (int s = threadIdx.x; s < S; s += kBlock) h[s] = 0;
   if (threadIdx.x == 0) nu = 0;
   __syncthreads();
-  const int base = blockIdx.x * kDispatchChunk;
-  for (int i = threadIdx.x; i < kDispatchChunk; i += kBlock) {
+  const int base = blockIdx.x * chunk;
+  for (int i = threadIdx.x; i < chunk; i += kBlock) {
     const int p = base + i;
     if (p >= npairs) break;
     const int e = ids[p];
@@ -72,10 +72,16 @@ __global__ __launch_bounds__(1024) void scan_kernel(int32_t* __restrict__ hist,
   if (s == 0) nu = 0;
   int total = 0;
   if (s < S) {
-    for (int c = 0; c < nchunks; ++c) {
-      const int v = hist[(size_t)c * S + s];
-      hist[(size_t)c * S + s] = total;  // base within the slot, made absolute below
-      total += v;
+    // Loads of 8 chunks are issued together; the running sum is sequential.
+    for (int c0 = 0; c0 < nchunks; c0 += 8) {
+      int v[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) v[i] = (c0 + i < nchunks) ? hist[(size_t)(c0 + i) * S + s] : 0;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        if (c0 + i < nchunks) hist[(size_t)(c0 + i) * S + s] = total;  // made absolute below
+        total += v[i];
+      }
     }
   }
   int part = 0;
@@ -96,7 +102,14 @@ __global__ __launch_bounds__(1024) void scan_kernel(int32_t* __restrict__ hist,
   if (s < S) {
     counts[s] = total;
     offsets[s] = excl;
-    for (int c = 0; c < nchunks; ++c) hist[(size_t)c * S + s] += excl;
+    for (int c0 = 0; c0 < nchunks; c0 += 8) {
+      int v[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) v[i] = (c0 + i < nchunks) ? hist[(size_t)(c0 + i) * S + s] : 0;
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+        if (c0 + i < nchunks) hist[(size_t)(c0 + i) * S + s] = v[i] + excl;
+    }
   }
   if (s == S - 1) offsets[S] = incl;
   __syncthreads();
@@ -107,21 +120,23 @@ __global__ __launch_bounds__(kBlock) void scatter_kernel(const int32_t* __restri
                                                          int npairs, int S,
                                                          const int32_t* __restrict__ base,
                                                          int32_t* __restrict__ perm,
-                                                         int32_t* __restrict__ pair_row) {
+                                                         int32_t* __restrict__ pair_row,
+                                                         int chunk) {
   constexpr int kWaves = kBlock / kWave;
-  constexpr int kQuarter = kDispatchChunk / kWaves;
   __shared__ int cnt[kWaves][kMaxS];
   const int wave = threadIdx.x / kWave;
   const int lane = lane_id();
+  // The chunk's pairs are split evenly (in multiples of 64) over the waves.
+  const int c0 = blockIdx.x * chunk;
+  const int n_c = min(chunk, npairs - c0);
+  const int span = ((n_c + kWaves * kWave - 1) / (kWaves * kWave)) * kWave;
+  const int p0 = c0 + wave * span;
+  const int p1 = min(c0 + n_c, p0 + span);
   for (int i = threadIdx.x; i < kWaves * kMaxS; i += kBlock) (&cnt[0][0])[i] = 0;
   __syncthreads();
-  const int p0 = blockIdx.x * kDispatchChunk + wave * kQuarter;
-  for (int i = lane; i < kQuarter; i += kWave) {
-    const int p = p0 + i;
-    if (p < npairs) {
-      const int s = pair_slot[p];
-      if (s >= 0) atomicAdd(&cnt[wave][s], 1);
-    }
+  for (int p = p0 + lane; p < p1; p += kWave) {
+    const int s = pair_slot[p];
+    if (s >= 0) atomicAdd(&cnt[wave][s], 1);
   }
   __syncthreads();
   for (int s = threadIdx.x; s < S; s += kBlock) {
@@ -134,10 +149,10 @@ __global__ __launch_bounds__(kBlock) void scatter_kernel(const int32_t* __restri
   }
   __syncthreads();
   const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-  for (int g = 0; g < kQuarter; g += kWave) {
-    const int p = p0 + g + lane;
+  for (int g = p0; g < p1; g += kWave) {
+    const int p = g + lane;
     int s = -1;
-    if (p < npairs) {
+    if (p < p1) {
       s = pair_slot[p];
       if (s < 0) pair_row[p] = -1;
     }
@@ -174,9 +189,16 @@ __global__ __launch_bounds__(kBlock) void gather_kernel(const uint4* __restrict_
 
 }  // namespace
 
+int dispatch_chunk(long npairs) {
+  const long per = (npairs + kDispatchChunks - 1) / kDispatchChunks;
+  const long c = (per + 255) / 256 * 256;
+  return (int)(c < 256 ? 256 : c);
+}
+
 size_t dispatch_workspace_bytes(int T, int k, int S) {
   const size_t npairs = (size_t)T * k;
-  const size_t nchunks = (npairs + kDispatchChunk - 1) / kDispatchChunk;
+  const int chunk = dispatch_chunk((long)npairs);
+  const size_t nchunks = (npairs + chunk - 1) / chunk;
   const size_t hist = nchunks * (size_t)S * sizeof(int32_t);
   return ((hist + 255) & ~(size_t)255) + ((nchunks * sizeof(int32_t) + 255) & ~(size_t)255) + 256;
 }
@@ -187,19 +209,20 @@ hipError_t launch_remap_dispatch(const int32_t* ids, int T, int k, const int32_t
                                  int32_t* perm, int32_t* pair_row, uint16_t* x_perm,
                                  int32_t* n_unserved, void* ws, hipStream_t stream) {
   const int npairs = T * k;
-  const int nchunks = (npairs + kDispatchChunk - 1) / kDispatchChunk;
+  const int chunk = dispatch_chunk(npairs);
+  const int nchunks = (npairs + chunk - 1) / chunk;
   const size_t hist_bytes = ((size_t)nchunks * S * sizeof(int32_t) + 255) & ~(size_t)255;
   int32_t* hist = static_cast<int32_t*>(ws);
   int32_t* unserved_chunk = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + hist_bytes);
   if (nchunks > 0) {
     hipLaunchKernelGGL(remap_count_kernel, dim3(nchunks), dim3(kBlock), 0, stream, ids, npairs, ert,
-                       E, R, alive, S, pair_slot, hist, unserved_chunk);
+                       E, R, alive, S, pair_slot, hist, unserved_chunk, chunk);
   }
   hipLaunchKernelGGL(scan_kernel, dim3(1), dim3(1024), 0, stream, hist, unserved_chunk, nchunks, S,
                      counts, offsets, n_unserved);
   if (nchunks > 0) {
     hipLaunchKernelGGL(scatter_kernel, dim3(nchunks), dim3(kBlock), 0, stream, pair_slot, npairs, S,
-                       hist, perm, pair_row);
+                       hist, perm, pair_row, chunk);
     if (x_perm) {
       const int nch = d / 8;
       const long maxq = (long)npairs * nch;

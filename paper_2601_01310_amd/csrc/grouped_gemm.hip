@@ -146,11 +146,15 @@ __device__ __forceinline__ bool map_tile(const int32_t* __restrict__ offsets, in
 // A (activation) tiles are double-buffered and B (weight) tiles triple-
 // buffered: weight slices are first touched in HBM, so they are requested
 // two stages ahead; activation slices are reused from cache.
-template <int BM, int BN, int BK, int WM, int WN, bool SWIGLU>
+//
+// GATHER: the activation rows are not pre-permuted; row r of the grouped
+// matrix is row perm[r] / kq of A (the token of routed pair perm[r]), read
+// in place through a buffer resource over all A_rows rows of A.
+template <int BM, int BN, int BK, int WM, int WN, bool SWIGLU, bool GATHER>
 __global__ __launch_bounds__(64 * WM * WN) void grouped_gemm_kernel(
     const uint16_t* __restrict__ A, const int32_t* __restrict__ offsets, int S,
     const uint16_t* __restrict__ B, int K, int NW, int I, uint16_t* __restrict__ C, int ldc,
-    int NT) {
+    int NT, const int32_t* __restrict__ perm, int kq, int A_rows) {
   constexpr int NWAVE = WM * WN;
   constexpr int MB = BM / WM / 32;          // 32-row blocks per wave
   constexpr int NB = BN / WN / 32;          // 32-col blocks per wave
@@ -180,7 +184,9 @@ __global__ __launch_bounds__(64 * WM * WN) void grouped_gemm_kernel(
   // row l / CH, so it fetches the global chunk that the swizzle puts there.
   const size_t b_row0 = (size_t)slot * NW + (SWIGLU ? nt * (BN / 2) : nt * BN);
   // Rows past the group's end read as zeros (their results are never stored).
-  const __amdgpu_buffer_rsrc_t a_rsrc = make_rsrc(A + (size_t)row0 * K, (uint32_t)rows * K * 2);
+  const __amdgpu_buffer_rsrc_t a_rsrc =
+      GATHER ? make_rsrc(A, (uint32_t)A_rows * K * 2)
+             : make_rsrc(A + (size_t)row0 * K, (uint32_t)rows * K * 2);
   const __amdgpu_buffer_rsrc_t b_rsrc = make_rsrc(
       B + b_row0 * K, (uint32_t)min((size_t)0x7fffffff, ((size_t)(slot + 1) * NW - b_row0) * K * 2));
   int a_off[AI], b_off[BI];  // byte offsets
@@ -188,7 +194,12 @@ __global__ __launch_bounds__(64 * WM * WN) void grouped_gemm_kernel(
   for (int i = 0; i < AI; ++i) {
     const int r = wave * (BM / NWAVE) + i * RPI + lane / CH;
     const int c = (lane % CH) ^ swz<CH>(r);
-    a_off[i] = (r * K + c * 8) * 2;
+    if (GATHER) {
+      // rows past the group's end get an offset beyond the resource: zeros
+      a_off[i] = (r < rows) ? ((perm[row0 + r] / kq) * K + c * 8) * 2 : (int)0x80000000u;
+    } else {
+      a_off[i] = (r * K + c * 8) * 2;
+    }
   }
 #pragma unroll
   for (int i = 0; i < BI; ++i) {
@@ -360,15 +371,17 @@ __global__ __launch_bounds__(64 * WM * WN) void grouped_gemm_kernel(
   }
 }
 
-template <int BM, int BN, int BK, int WM, int WN, bool SWIGLU>
+template <int BM, int BN, int BK, int WM, int WN, bool SWIGLU, bool GATHER = false>
 hipError_t launch_grouped(const uint16_t* A, const int32_t* offsets, int S, int max_rows,
                           const uint16_t* B, int K, int NW, int I, uint16_t* C, int ldc, int NT,
-                          hipStream_t stream) {
+                          hipStream_t stream, const int32_t* perm = nullptr, int kq = 1,
+                          int A_rows = 0) {
   // Bound on the tile count: sum_s ceil(count_s / BM) <= ceil(max_rows / BM) + S.
   const long bound = ((long)(max_rows + BM - 1) / BM + S) * NT;
   const long grid = (bound + kXcds - 1) / kXcds * kXcds;
-  hipLaunchKernelGGL((grouped_gemm_kernel<BM, BN, BK, WM, WN, SWIGLU>), dim3((unsigned)grid),
-                     dim3(64 * WM * WN), 0, stream, A, offsets, S, B, K, NW, I, C, ldc, NT);
+  hipLaunchKernelGGL((grouped_gemm_kernel<BM, BN, BK, WM, WN, SWIGLU, GATHER>),
+                     dim3((unsigned)grid), dim3(64 * WM * WN), 0, stream, A, offsets, S, B, K, NW,
+                     I, C, ldc, NT, perm, kq, A_rows);
   return hipGetLastError();
 }
 
@@ -381,6 +394,15 @@ hipError_t launch_ffn_gateup(const uint16_t* x_perm, const int32_t* offsets, int
   if (max_rows == 0) return hipSuccess;
   return launch_grouped<kBM, kBN, kBK, kWM, kWN, true>(x_perm, offsets, S, max_rows, w13, d,
                                                        2 * I, I, h, I, (2 * I) / kBN, stream);
+}
+
+hipError_t launch_ffn_gateup_gather(const uint16_t* x, int T, const int32_t* perm, int k,
+                                    const int32_t* offsets, int S, int max_rows,
+                                    const uint16_t* w13, int d, int I, uint16_t* h,
+                                    hipStream_t stream) {
+  if (max_rows == 0) return hipSuccess;
+  return launch_grouped<kBM, kBN, kBK, kWM, kWN, true, true>(
+      x, offsets, S, max_rows, w13, d, 2 * I, I, h, I, (2 * I) / kBN, stream, perm, k, T);
 }
 
 hipError_t launch_ffn_down(const uint16_t* h, const int32_t* offsets, int S, int max_rows,

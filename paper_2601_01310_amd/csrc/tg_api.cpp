@@ -112,7 +112,10 @@ EwLayout ew_layout(const tg_ew_args* a, char* base) {
   L.n_unserved = reinterpret_cast<int32_t*>(take(4));
   L.perm = reinterpret_cast<int32_t*>(take(np * 4));
   L.dispatch_ws = take(tg::dispatch_workspace_bytes(a->T, a->k, a->S));
-  L.x_perm = reinterpret_cast<uint16_t*>(take(np * a->d * 2));
+  // The permuted copy of x is only needed when x is too large to be read in
+  // place (see tg_ew_forward).
+  const bool in_place = 2LL * a->T * a->d < (1LL << 31);
+  L.x_perm = reinterpret_cast<uint16_t*>(take(in_place ? 0 : np * a->d * 2));
   L.h = reinterpret_cast<uint16_t*>(take(np * a->I * 2));
   L.y = reinterpret_cast<uint16_t*>(take(np * a->d * 2));
   L.bytes = off;
@@ -261,13 +264,20 @@ static tg_status ew_forward(const tg_ew_args* a, void* ws, size_t ws_bytes, void
     e = tg::launch_gate_topk(a->w_gate ? a->x : nullptr, a->w_gate, a->logits_in, a->T, a->d, a->E,
                              a->k, nullptr, ids, w, s);
   mark(1);
+  // The gate/up GEMM reads the token rows in place through perm when x is
+  // addressable with 32-bit byte offsets; otherwise they are gathered first.
+  const bool in_place = 2LL * a->T * a->d < (1LL << 31);
   if (e == hipSuccess)
-    e = tg::launch_remap_dispatch(ids, a->T, a->k, a->ert, a->E, a->R, a->slot_alive, a->S, a->x,
-                                  a->d, pair_slot, counts, offsets, L.perm, pair_row, L.x_perm,
-                                  n_unserved, L.dispatch_ws, s);
+    e = tg::launch_remap_dispatch(ids, a->T, a->k, a->ert, a->E, a->R, a->slot_alive, a->S,
+                                  in_place ? nullptr : a->x, a->d, pair_slot, counts, offsets,
+                                  L.perm, pair_row, in_place ? nullptr : L.x_perm, n_unserved,
+                                  L.dispatch_ws, s);
   mark(2);
   if (e == hipSuccess)
-    e = tg::launch_ffn_gateup(L.x_perm, offsets, a->S, max_rows, a->w13, a->d, a->I, L.h, s);
+    e = in_place ? tg::launch_ffn_gateup_gather(a->x, a->T, L.perm, a->k, offsets, a->S, max_rows,
+                                                a->w13, a->d, a->I, L.h, s)
+                 : tg::launch_ffn_gateup(L.x_perm, offsets, a->S, max_rows, a->w13, a->d, a->I,
+                                         L.h, s);
   mark(3);
   if (e == hipSuccess)
     e = tg::launch_ffn_down(L.h, offsets, a->S, max_rows, a->w2, a->d, a->I, L.y, s);

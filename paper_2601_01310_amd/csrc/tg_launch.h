@@ -12,9 +12,11 @@ hipError_t launch_gate_topk(const uint16_t* x, const uint16_t* wg, const float* 
                             int d, int E, int k, float* logits_out, int32_t* ids, float* w,
                             hipStream_t stream);
 
-// Pairs are processed in chunks of kDispatchChunk; the workspace holds one
-// S-wide histogram per chunk and one unserved count per chunk.
-constexpr int kDispatchChunk = 4096;
+// Pairs are processed in about kDispatchChunks chunks (each a multiple of
+// 256 pairs, at least 256); the workspace holds one S-wide histogram and one
+// unserved count per chunk.
+constexpr int kDispatchChunks = 64;
+int dispatch_chunk(long npairs);
 size_t dispatch_workspace_bytes(int T, int k, int S);
 hipError_t launch_remap_dispatch(const int32_t* ids, int T, int k, const int32_t* ert, int E, int R,
                                  const uint8_t* alive, int S, const uint16_t* x, int d,
@@ -24,6 +26,12 @@ hipError_t launch_remap_dispatch(const int32_t* ids, int T, int k, const int32_t
 
 hipError_t launch_ffn_gateup(const uint16_t* x_perm, const int32_t* offsets, int S, int max_rows,
                              const uint16_t* w13, int d, int I, uint16_t* h, hipStream_t stream);
+// Same as launch_ffn_gateup with the activation rows gathered in place:
+// grouped row r is row perm[r] / k of x [T, d] (requires T * d * 2 < 2^31).
+hipError_t launch_ffn_gateup_gather(const uint16_t* x, int T, const int32_t* perm, int k,
+                                    const int32_t* offsets, int S, int max_rows,
+                                    const uint16_t* w13, int d, int I, uint16_t* h,
+                                    hipStream_t stream);
 hipError_t launch_ffn_down(const uint16_t* h, const int32_t* offsets, int S, int max_rows,
                            const uint16_t* w2, int d, int I, uint16_t* y, hipStream_t stream);
 hipError_t launch_expert_ffn(const uint16_t* x_perm, const int32_t* offsets, int S, int max_rows,
