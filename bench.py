@@ -22,6 +22,23 @@ sys.path.insert(0, ROOT)
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 STAGES = ["gate", "dispatch", "ffn_gateup", "ffn_down", "combine"]
+GEMM_SRC = os.path.join(ROOT, "paper_2601_01310_amd", "csrc", "grouped_gemm.hip")
+TRAFFIC = os.path.join(ROOT, "profiles", "gemm_gateup_mixtral_traffic.json")
+
+
+def measured_traffic(workload: str):
+    """HBM-side bytes per dispatch of the gate/up GEMM from the committed
+    rocprofv3 FETCH_SIZE / WRITE_SIZE runs, or None when they were taken on
+    another workload or before the kernel source last changed."""
+    import hashlib
+    try:
+        rec = json.load(open(TRAFFIC))
+    except (OSError, ValueError):
+        return None
+    sha = hashlib.sha256(open(GEMM_SRC, "rb").read()).hexdigest()
+    if rec.get("source_sha256") != sha or rec.get("workload") != workload:
+        return None
+    return rec.get("traffic_bytes_per_dispatch")
 
 
 class HipEvents:
@@ -93,6 +110,9 @@ def main():
     ap.add_argument("--failover", action="store_true",
                     help="time the run with the workload's failed primaries rerouted to shadows")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calib-copy", action="store_true",
+                    help="first copy a 1 GiB device buffer 3 times (a plain copy of known size "
+                         "that calibrates the FETCH_SIZE / WRITE_SIZE counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the expert-parallel "
@@ -106,6 +126,13 @@ def main():
     tg.load()
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.calib_copy:
+        src = torch.ones(1 << 30, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     wl = synth.make(args.workload, device=dev)
     alive = wl.alive_after_failure() if args.failover else wl.alive
     f = tg.EwForward(wl, alive)
@@ -152,7 +179,8 @@ def main():
                    "routed_pairs": P},
         "roofline": {"bound": "mfma", "kernel": "grouped_gemm gate/up + SwiGLU",
                      "achieved": gemm1_tflops, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                     "frac": gemm1_tflops / PEAK_BF16_TFLOPS, "traffic": None},
+                     "frac": gemm1_tflops / PEAK_BF16_TFLOPS,
+                     "traffic": measured_traffic(args.workload)},
         "stages_ms": dict(zip(STAGES, stage_ms)),
         "expert_ffn_tflops": ffn_tflops,
     }
