@@ -101,6 +101,137 @@ def cpu_baseline(wl, n_tokens: int = 1024):
                       f"per-token oracle incl. widening the touched slots' bf16 weights; {dt:.1f} s"}
 
 
+def _ffn_buffers(d, I, S, max_rows, dev, seed=0):
+    import torch
+    g = torch.Generator(device=dev)
+    g.manual_seed(seed)
+    x = (torch.randn((max_rows, d), generator=g, device=dev)).to(torch.bfloat16)
+    w13 = (torch.randn((S, 2 * I, d), generator=g, device=dev) * 0.02).to(torch.bfloat16)
+    w2 = (torch.randn((S, d, I), generator=g, device=dev) * 0.02).to(torch.bfloat16)
+    h = torch.empty((max_rows, I), dtype=torch.bfloat16, device=dev)
+    y = torch.empty((max_rows, d), dtype=torch.bfloat16, device=dev)
+    return x, w13, w2, h, y
+
+
+def _offsets(counts, dev):
+    import torch
+    off = [0]
+    for c in counts:
+        off.append(off[-1] + c)
+    return torch.tensor(off, dtype=torch.int32, device=dev)
+
+
+def expert_batch_knee(dev, reps=20):
+    """Expert FFN latency and throughput against the expert batch size (the
+    paper's expert-batch-size knee, App. B), through tg_expert_ffn_grouped with
+    all rows in one slot. Slots rotate over 8 copies so the weights come from
+    HBM, not from the 256 MB Infinity Cache."""
+    import torch
+
+    from paper_2601_01310_amd import tg
+
+    hip = HipEvents()
+    out = []
+    for name, d, I in (("mixtral expert", 4096, 14336), ("deepseek-v3 expert", 7168, 2048)):
+        S = 8
+        Ms = [1, 2, 4, 8, 16, 32, 64, 128, 256, 512, 1024, 2048, 4096]
+        x, w13, w2, h, y = _ffn_buffers(d, I, S, max(Ms), dev)
+        for M in Ms:
+            offs = [_offsets([M if s == j else 0 for s in range(S)], dev) for j in range(S)]
+            for j in range(3):
+                tg.tg_expert_ffn_grouped(x, offs[j % S], S, M, w13, w2, d, I, h, y)
+            ev = hip.create(2)
+            torch.cuda.synchronize()
+            from ctypes import c_void_p
+            hip.hip.hipEventRecord(c_void_p(ev[0]), c_void_p(torch.cuda.current_stream().cuda_stream))
+            for j in range(reps):
+                tg.tg_expert_ffn_grouped(x, offs[j % S], S, M, w13, w2, d, I, h, y)
+            hip.hip.hipEventRecord(c_void_p(ev[1]), c_void_p(torch.cuda.current_stream().cuda_stream))
+            torch.cuda.synchronize()
+            us = hip.elapsed_ms(ev[0], ev[1]) * 1e3 / reps
+            hip.destroy(ev)
+            flops = 6.0 * d * I * M
+            wbytes = 3.0 * d * I * 2
+            rec = dict(expert=name, rows=M, us=us, tflops=flops / us / 1e6,
+                       weight_tbps=wbytes / us / 1e6, us_per_row=us / M)
+            out.append(rec)
+            print(json.dumps(rec), flush=True)
+        del x, w13, w2, h, y
+        torch.cuda.empty_cache()
+    return out
+
+
+def shadow_interference(dev, reps=20):
+    """Loaded-but-idle shadow slot vs a single expert vs two experts run
+    concurrently on two streams with the same total batch (App. D)."""
+    import torch
+    from ctypes import c_void_p
+
+    from paper_2601_01310_amd import tg
+
+    hip = HipEvents()
+    d, I, M = 4096, 14336, 512
+    S = 8
+    x, w13, w2, h, y = _ffn_buffers(d, I, S, M, dev)
+    h2 = torch.empty_like(h)
+    y2 = torch.empty_like(y)
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+
+    def timed(fn):
+        for j in range(3):
+            fn(j)
+        torch.cuda.synchronize()
+        ev = hip.create(2)
+        cur = torch.cuda.current_stream()
+        hip.hip.hipEventRecord(c_void_p(ev[0]), c_void_p(cur.cuda_stream))
+        s1.wait_stream(cur)
+        s2.wait_stream(cur)
+        for j in range(reps):
+            fn(j)
+        cur.wait_stream(s1)
+        cur.wait_stream(s2)
+        hip.hip.hipEventRecord(c_void_p(ev[1]), c_void_p(cur.cuda_stream))
+        torch.cuda.synchronize()
+        us = hip.elapsed_ms(ev[0], ev[1]) * 1e3 / reps
+        hip.destroy(ev)
+        return us
+
+    one = [_offsets([M if s == j % 4 else 0 for s in range(4)], dev) for j in range(4)]
+    # slot j%4 active with M rows, plus 4 loaded shadow slots (copies) that stay idle
+    with_shadow = [_offsets([M if s == j % 4 else 0 for s in range(S)], dev) for j in range(4)]
+    half_a = [_offsets([M // 2 if s == (2 * j) % 8 else 0 for s in range(S)], dev) for j in range(4)]
+    half_b = [_offsets([M // 2 if s == (2 * j + 1) % 8 else 0 for s in range(S)], dev) for j in range(4)]
+    grouped = [_offsets([M // 2 if s in ((2 * j) % 8, (2 * j + 1) % 8) else 0 for s in range(S)], dev)
+               for j in range(4)]
+
+    def single(j):
+        tg.tg_expert_ffn_grouped(x, one[j % 4], 4, M, w13, w2, d, I, h, y)
+
+    def shadow_loaded(j):
+        tg.tg_expert_ffn_grouped(x, with_shadow[j % 4], S, M, w13, w2, d, I, h, y)
+
+    def concurrent(j):
+        with torch.cuda.stream(s1):
+            tg.tg_expert_ffn_grouped(x, half_a[j % 4], S, M // 2, w13, w2, d, I, h, y, stream=s1)
+        with torch.cuda.stream(s2):
+            tg.tg_expert_ffn_grouped(x, half_b[j % 4], S, M // 2, w13, w2, d, I, h2, y2, stream=s2)
+
+    def two_in_one_launch(j):
+        tg.tg_expert_ffn_grouped(x, grouped[j % 4], S, M, w13, w2, d, I, h, y)
+
+    cases = (("single_expert_us", single), ("single_plus_idle_shadows_us", shadow_loaded),
+             ("two_experts_two_streams_us", concurrent),
+             ("two_experts_one_grouped_launch_us", two_in_one_launch))
+    # Two passes over all cases; the first brings clocks and caches to a
+    # steady state and is discarded.
+    for _ in range(2):
+        res = {"rows_total": M, "expert": "mixtral expert (d=4096, I=14336)"}
+        for name, fn in cases:
+            res[name] = timed(fn)
+    print(json.dumps(res), flush=True)
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -110,6 +241,11 @@ def main():
     ap.add_argument("--failover", action="store_true",
                     help="time the run with the workload's failed primaries rerouted to shadows")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--knee", action="store_true",
+                    help="expert FFN time against the expert batch size (prints one JSON line per "
+                         "point instead of the benchmark line)")
+    ap.add_argument("--shadow", action="store_true",
+                    help="idle-shadow / concurrent-expert interference check (one JSON line)")
     ap.add_argument("--calib-copy", action="store_true",
                     help="first copy a 1 GiB device buffer 3 times (a plain copy of known size "
                          "that calibrates the FETCH_SIZE / WRITE_SIZE counters)")
@@ -133,6 +269,12 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
+    if args.knee:
+        expert_batch_knee(dev)
+        return
+    if args.shadow:
+        shadow_interference(dev)
+        return
     wl = synth.make(args.workload, device=dev)
     alive = wl.alive_after_failure() if args.failover else wl.alive
     f = tg.EwForward(wl, alive)

@@ -94,6 +94,65 @@ def test_ffn_entry_point_rows_independent_of_position(tiny):
     G.assert_close_bf16(Y[13:53], ref, "y slot 3")
 
 
+def test_ffn_tile_shapes_give_identical_bits(tiny):
+    """The row bound selects the tile shape (32-row tiles when it allows at
+    most 32 rows per slot on average, else 256-row tiles); both shapes give
+    the same bits on the same rows, across full tiles and ragged tails."""
+    d, I, S = tiny.d, tiny.I, tiny.S
+    cnt = torch.tensor([0, 33, 1, 70, 0, 64, 31, 40, 29, 32], dtype=torch.int32)
+    assert cnt.numel() == S
+    P = int(cnt.sum())                     # 300 <= 32 * S: small tiles at max_rows = P
+    big = 32 * S + 1                       # large tiles
+    g = torch.Generator().manual_seed(7)
+    x_perm = torch.randn((big, d), generator=g).to(torch.bfloat16).to(DEV)
+    offsets = torch.zeros(S + 1, dtype=torch.int32)
+    offsets[1:] = torch.cumsum(cnt, 0)
+    offsets = offsets.to(DEV)
+    outs = []
+    for max_rows in (P, big):
+        h = torch.zeros((big, I), dtype=torch.bfloat16, device=DEV)
+        y = torch.zeros((big, d), dtype=torch.bfloat16, device=DEV)
+        tg.tg_expert_ffn_grouped(x_perm, offsets, S, max_rows, tiny.w13, tiny.w2, d, I, h, y)
+        torch.cuda.synchronize()
+        outs.append((u16(h[:P]), u16(y[:P])))
+    assert np.array_equal(outs[0][0], outs[1][0]), "h differs between tile shapes"
+    assert np.array_equal(outs[0][1], outs[1][1]), "y differs between tile shapes"
+    o = int(offsets[3])
+    ref = O.expert_ffn(u16(x_perm[o:o + 70]), u16(tiny.w13[3]), u16(tiny.w2[3]))[1]
+    G.assert_close_bf16(outs[0][1][o:o + 70], ref, "y slot 3")
+
+
+def test_ffn_partial_last_round_split_matches_oracle():
+    """d = 4096 gives the down projection 16 column panels of 256; 17 row
+    blocks of 256 make 272 tiles, so 16 tiles spill past the 256 CUs of one
+    round and run as quarter tiles. Every row is checked against the oracle,
+    and rows of a layout without that spill (the last slot empty: 224
+    tiles) give the same bits."""
+    d, I, S = 4096, 128, 10
+    counts = [300, 256, 1, 513, 0, 200, 255, 257, 700, 530]  # 17 row blocks of 256
+    g = torch.Generator().manual_seed(11)
+    x = torch.randn((sum(counts), d), generator=g).to(torch.bfloat16).to(DEV)
+    w13 = (torch.randn((S, 2 * I, d), generator=g) * 0.02).to(torch.bfloat16).to(DEV)
+    w2 = (torch.randn((S, d, I), generator=g) * 0.02).to(torch.bfloat16).to(DEV)
+    ys = []
+    for cnt in (counts, counts[:-1] + [0]):
+        off = np.concatenate([[0], np.cumsum(cnt)]).astype(np.int32)
+        P = int(off[-1])
+        h = torch.zeros((P, I), dtype=torch.bfloat16, device=DEV)
+        y = torch.zeros((P, d), dtype=torch.bfloat16, device=DEV)
+        tg.tg_expert_ffn_grouped(x[:P].contiguous(), torch.from_numpy(off).to(DEV), S, P, w13, w2,
+                                 d, I, h, y)
+        torch.cuda.synchronize()
+        ys.append((off, u16(y)))
+    off, Y = ys[0]
+    for s in range(S):
+        if counts[s]:
+            ref = O.expert_ffn(u16(x[off[s]:off[s + 1]]), u16(w13[s]), u16(w2[s]))[1]
+            G.assert_close_bf16(Y[off[s]:off[s + 1]], ref, f"y slot {s}")
+    n = int(ys[1][0][-1])
+    assert np.array_equal(Y[:n], ys[1][1]), "rows differ between layouts with and without a spill"
+
+
 def test_repeat_calls_are_bit_identical(tiny):
     a, b = G.run_fused(tiny), G.run_fused(tiny)
     for key in a:
