@@ -21,6 +21,7 @@ sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+RIDGE_FLOP_PER_BYTE = PEAK_BF16_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9)
 STAGES = ["gate", "dispatch", "ffn_gateup", "ffn_down", "combine"]
 GEMM_SRC = os.path.join(ROOT, "paper_2601_01310_amd", "csrc", "grouped_gemm.hip")
 TRAFFIC = os.path.join(ROOT, "profiles", "gemm_gateup_mixtral_traffic.json")
@@ -235,8 +236,8 @@ def shadow_interference(dev, reps=20):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="mixtral")
     ap.add_argument("--failover", action="store_true",
                     help="time the run with the workload's failed primaries rerouted to shadows")
@@ -281,27 +282,59 @@ def main():
     hip = HipEvents()
     stream = torch.cuda.current_stream()
 
+    def timed_steps(n):
+        """n steps of the whole path; per-stage and per-step event times (ms)
+        and the host wall time per step."""
+        evs = hip.create(6 * n)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for i in range(n):
+            tg.tg_ew_forward_timed(f.args, f.ws, f.ws_bytes, evs[6 * i:6 * i + 6], stream)
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        stages = [[hip.elapsed_ms(evs[6 * i + j], evs[6 * i + j + 1]) for j in range(5)]
+                  for i in range(n)]
+        hip.destroy(evs)
+        return stages, (t1 - t0) * 1e3 / n
+
     for _ in range(args.warmup):
         f(stream)
-    evs = hip.create(6 * args.steps)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for i in range(args.steps):
-        tg.tg_ew_forward_timed(f.args, f.ws, f.ws_bytes, evs[6 * i:6 * i + 6], stream)
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    stage_ms = [0.0] * 5
-    for i in range(args.steps):
-        e = evs[6 * i:6 * i + 6]
-        for j in range(5):
-            stage_ms[j] += hip.elapsed_ms(e[j], e[j + 1]) / args.steps
-    hip.destroy(evs)
-
-    ms = (t1 - t0) * 1e3 / args.steps
+    per_step, ms = timed_steps(args.steps)
+    stage_ms = [sum(st[j] for st in per_step) / args.steps for j in range(5)]
+    step_ev = sorted(sum(st) for st in per_step)
     P = int(f.slot_offsets[-1])
+    counts = f.slot_counts.cpu()
+    touched = int((counts > 0).sum())
+
+    failover = None
+    if not args.failover and not torch.equal(wl.alive_after_failure(), wl.alive):
+        # The same inputs with the workload's failed primaries rerouted to
+        # their shadows: the rerouted run should cost the same.
+        f.set_alive(wl.alive_after_failure())
+        for _ in range(args.warmup):
+            f(stream)
+        fo_steps, fo_ms = timed_steps(args.steps)
+        fo_ev = sorted(sum(st) for st in fo_steps)
+        failover = {"ms_per_step": fo_ms, "step_ms_p50": fo_ev[len(fo_ev) // 2],
+                    "routed_pairs": int(f.slot_offsets[-1])}
+        f.set_alive(wl.alive)
+
     d, I = wl.d, wl.I
     gemm1_flop = 4.0 * d * I * P
-    gemm1_tflops = gemm1_flop / (stage_ms[2] * 1e-3) / 1e12
+    gemm1_s = stage_ms[2] * 1e-3
+    # Algorithmic bytes of the gate/up GEMM: the touched slots' W1/W3, the
+    # routed rows of x and h.
+    gemm1_bytes = touched * 2.0 * I * d * 2 + P * d * 2.0 + P * I * 2.0
+    if gemm1_flop / max(gemm1_bytes, 1.0) >= RIDGE_FLOP_PER_BYTE:
+        achieved = gemm1_flop / gemm1_s / 1e12
+        roof = {"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
+                "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS}
+    else:
+        achieved = gemm1_bytes / gemm1_s / 1e9
+        roof = {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": achieved / PEAK_HBM_GBS}
+    roof = {"bound": roof["bound"], "kernel": "grouped_gemm gate/up + SwiGLU", **roof,
+            "traffic": measured_traffic(args.workload)}
     ffn_tflops = 6.0 * d * I * P / ((stage_ms[2] + stage_ms[3]) * 1e-3) / 1e12
     line = {
         "metric": "routed token-expert pairs/sec for EW forward",
@@ -318,14 +351,15 @@ def main():
         "data": "synthetic",
         "config": {"workload": f"{args.workload}: T={wl.T} d={d} E={wl.E} top-{wl.k} I={I} "
                                f"slots={wl.S}" + (" failover" if args.failover else ""),
-                   "routed_pairs": P},
-        "roofline": {"bound": "mfma", "kernel": "grouped_gemm gate/up + SwiGLU",
-                     "achieved": gemm1_tflops, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                     "frac": gemm1_tflops / PEAK_BF16_TFLOPS,
-                     "traffic": measured_traffic(args.workload)},
+                   "routed_pairs": P, "touched_slots": touched},
+        "roofline": roof,
+        "step_ms_p50": step_ev[len(step_ev) // 2],
+        "step_ms_mean": sum(step_ev) / len(step_ev),
         "stages_ms": dict(zip(STAGES, stage_ms)),
         "expert_ffn_tflops": ffn_tflops,
     }
+    if failover is not None:
+        line["failover"] = failover
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(wl)
     print(json.dumps(line), flush=True)
