@@ -233,6 +233,46 @@ def shadow_interference(dev, reps=20):
     return res
 
 
+def replay_cost(wl, steps, warmup):
+    """Cost of replaying the pairs of the workload's failed primaries on
+    their shadows after a completed forward (§5.1), against the forward
+    itself; HIP events around each call."""
+    import torch
+    from ctypes import c_void_p
+
+    from paper_2601_01310_amd import tg
+
+    hip = HipEvents()
+    stream = torch.cuda.current_stream()
+    f = tg.EwForward(wl, keep_y=True)
+    alive1 = wl.alive_after_failure()
+
+    def timed(fn):
+        for _ in range(warmup):
+            fn()
+        ev = hip.create(2 * steps)
+        torch.cuda.synchronize()
+        for i in range(steps):
+            hip.hip.hipEventRecord(c_void_p(ev[2 * i]), c_void_p(stream.cuda_stream))
+            fn()
+            hip.hip.hipEventRecord(c_void_p(ev[2 * i + 1]), c_void_p(stream.cuda_stream))
+        torch.cuda.synchronize()
+        us = sorted(hip.elapsed_ms(ev[2 * i], ev[2 * i + 1]) * 1e3 for i in range(steps))
+        hip.destroy(ev)
+        return us[len(us) // 2]
+
+    fwd_us = timed(lambda: f(stream))
+    f(stream)
+    rep_us = timed(lambda: f.replay(alive1, stream))
+    _, n_rep, _ = f.replay(alive1, stream)
+    torch.cuda.synchronize()
+    res = {"workload": wl.name, "failed_slots": int((wl.alive != alive1).sum()),
+           "pairs_replayed": int(n_rep[0]), "routed_pairs": int(f.slot_offsets[-1]),
+           "forward_us_p50": fwd_us, "replay_us_p50": rep_us}
+    print(json.dumps(res), flush=True)
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -247,6 +287,9 @@ def main():
                          "point instead of the benchmark line)")
     ap.add_argument("--shadow", action="store_true",
                     help="idle-shadow / concurrent-expert interference check (one JSON line)")
+    ap.add_argument("--replay", action="store_true",
+                    help="cost of replaying the failed primaries' pairs after a forward, against "
+                         "the forward (one JSON line)")
     ap.add_argument("--calib-copy", action="store_true",
                     help="first copy a 1 GiB device buffer 3 times (a plain copy of known size "
                          "that calibrates the FETCH_SIZE / WRITE_SIZE counters)")
@@ -277,6 +320,9 @@ def main():
         shadow_interference(dev)
         return
     wl = synth.make(args.workload, device=dev)
+    if args.replay:
+        replay_cost(wl, args.steps, args.warmup)
+        return
     alive = wl.alive_after_failure() if args.failover else wl.alive
     f = tg.EwForward(wl, alive)
     hip = HipEvents()

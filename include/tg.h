@@ -133,9 +133,16 @@ tg_status tg_combine(const uint16_t* y, const int32_t* pair_row, const float* to
  *
  * Gating input is either (x, w_gate) or logits_in (see tg_gate_topk).
  * Optional outputs (NULL = kept in the workspace only): topk_ids, topk_w,
- * pair_slot, slot_counts, slot_offsets, pair_row, n_unserved. out is
- * required. The workspace holds every intermediate, including the permuted
- * activations, h and y sized for T*k rows.
+ * pair_slot, slot_counts, slot_offsets, pair_row, n_unserved, and y, the
+ * per-pair expert outputs [T*k, d] bf16 in pair_row order (keep topk_ids,
+ * topk_w, pair_slot, pair_row and y to replay failed pairs later with
+ * tg_ew_replay). out is required. The workspace holds every other
+ * intermediate (h, and y when not given, sized for T*k rows).
+ *
+ * token_valid [T] uint8 (optional): the EW-side partial batch (§5.2). Tokens
+ * with 0 are not part of this batch: their pairs get pair_slot -2 and
+ * pair_row -1, are not counted in n_unserved, and their out rows are +0.
+ * The other tokens' results do not depend on the mask.
  */
 typedef struct {
   int T, d, E, k, I, S, R;
@@ -154,6 +161,8 @@ typedef struct {
   int32_t* slot_offsets;      /* [S+1] or NULL */
   int32_t* pair_row;          /* [T,k] or NULL */
   int32_t* n_unserved;        /* [1] or NULL */
+  uint16_t* y;                /* [T*k,d] bf16 or NULL */
+  const uint8_t* token_valid; /* [T] or NULL (all tokens in the batch) */
 } tg_ew_args;
 
 size_t tg_ew_forward_workspace(const tg_ew_args* a);
@@ -168,6 +177,80 @@ tg_status tg_ew_forward(const tg_ew_args* a, void* ws, size_t ws_bytes, void* st
  */
 tg_status tg_ew_forward_timed(const tg_ew_args* a, void* ws, size_t ws_bytes, void* stream,
                               void* const* events, int n_events);
+
+/*
+ * Replay of failed pairs (§5.1): after a forward, slots may fail (or be
+ * restored) before its result is used. Experts are stateless and
+ * deterministic, so a pair whose slot has failed is recomputed on the next
+ * live candidate of its expert from the same token row and merged into the
+ * output, without recomputing anything else.
+ *
+ * Inputs are the first pass's x, topk_ids, topk_w, pair_slot, pair_row and
+ * y (tg_ew_args fields), the ERT, the weights and the CURRENT slot_alive.
+ * A pair is replayed when its first-pass slot is no longer alive, or when it
+ * had no live local candidate, and its expert now has one; it is computed on
+ * the first live candidate. A pair whose first-pass slot failed and that has
+ * no live candidate left is dropped (the remaining weights are not
+ * renormalised). Every token with a replayed or dropped pair gets its out
+ * row re-formed (same float32 rank-order sum as tg_combine); other rows of
+ * out are not touched. When every candidate slot of an expert holds the same
+ * weights, out afterwards equals, bit for bit, what tg_ew_forward gives with
+ * the current slot_alive.
+ *
+ * Outputs: out [T,d] (in/out), and optionally replay_slot [T,k] (slot of
+ * each replayed pair, else -1), n_replayed [1], n_unserved [1] (pairs whose
+ * expert has local candidates, none alive now; as tg_ew_forward counts
+ * them). Pairs with pair_slot -2 (outside the batch) are never replayed.
+ */
+typedef struct {
+  int T, d, E, k, I, S, R;
+  const uint16_t* x;          /* [T,d] bf16, the first pass's token rows */
+  const int32_t* ert;         /* [E,R] */
+  const uint8_t* slot_alive;  /* [S], current */
+  const uint16_t* w13;        /* [S,2I,d] bf16 */
+  const uint16_t* w2;         /* [S,d,I] bf16 */
+  const int32_t* topk_ids;    /* [T,k], first pass */
+  const float* topk_w;        /* [T,k], first pass */
+  const int32_t* pair_slot;   /* [T,k], first pass */
+  const int32_t* pair_row;    /* [T,k], first pass */
+  const uint16_t* y;          /* [T*k,d] bf16, first pass */
+  uint16_t* out;              /* [T,d] bf16, in/out */
+  int32_t* replay_slot;       /* [T,k] or NULL */
+  int32_t* n_replayed;        /* [1] or NULL */
+  int32_t* n_unserved;        /* [1] or NULL */
+} tg_replay_args;
+
+size_t tg_ew_replay_workspace(const tg_replay_args* a);
+tg_status tg_ew_replay(const tg_replay_args* a, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * EW-side partial-batch trigger (§5.2): start the layer's expert work once
+ * a sufficient subset of attention workers (AWs) has delivered its tokens.
+ *
+ * The batch buffer x [T,d] holds the rows of A AWs as chunks: AW a's rows
+ * are chunk_rows[a] .. chunk_rows[a+1]-1 (chunk_rows [A+1] int32, device,
+ * non-decreasing; rows outside [0,T) are ignored, rows in no chunk are never
+ * in the batch). delivered [A] uint32 is nonzero once AW a's chunk has
+ * arrived; it may be device memory or host-visible memory that the
+ * transport writes while the trigger waits (read with system-scope loads).
+ * aw_alive [A] uint8 is 0 for AWs known to have failed.
+ *
+ * One kernel on `stream` polls delivered[] until (i) every AW with
+ * aw_alive[a] != 0 has delivered, or (ii) the rows of the live AWs that
+ * have delivered reach min_rows, or (iii) spin_limit polls (each followed by
+ * a short sleep, about 4 us) have passed: the probing window, after which
+ * live AWs that have not delivered are left out of this batch (treated as
+ * failed for this layer). It then writes token_valid [T] (1 for the rows of
+ * live AWs that had delivered at the deciding poll, else 0), ready to pass
+ * as tg_ew_args.token_valid to a forward enqueued after it, and status [4]
+ * int32 = {condition met (0, 1 or 2 for i, ii, iii), rows in the batch,
+ * AWs in the batch, polls made}. The kernel always ends after at most
+ * spin_limit polls. Limits: 1 <= A <= 1024, spin_limit >= 1.
+ */
+tg_status tg_batch_trigger(const uint32_t* delivered, const uint8_t* aw_alive,
+                           const int32_t* chunk_rows, int A, int T, int min_rows,
+                           long long spin_limit, uint8_t* token_valid, int32_t* status,
+                           void* stream);
 
 #ifdef __cplusplus
 }

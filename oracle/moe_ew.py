@@ -114,19 +114,24 @@ def gate_weights(logits: np.ndarray, ids: np.ndarray) -> np.ndarray:
 # ----------------------------------------------------------------------------
 
 
-def remap(ids: np.ndarray, ert: np.ndarray, alive: np.ndarray):
+def remap(ids: np.ndarray, ert: np.ndarray, alive: np.ndarray, token_valid=None):
     """pair_slot[t, j] = first candidate c of ert[ids[t, j]] with 0 <= c < S and alive[c].
 
     A pair whose expert lists at least one valid local candidate, none alive,
     is counted in ``n_unserved`` (it must be replayed on another EW); an
     expert with no valid local candidate belongs to another EW and is not
-    counted. Entries outside [0, S) are ignored.
+    counted. Entries outside [0, S) are ignored. Tokens with
+    ``token_valid[t] == 0`` are not in this batch (the EW started without
+    them, §5.2): their pairs get -2 and are not counted.
     """
     T, k = ids.shape
     S = alive.shape[0]
     pair_slot = np.full((T, k), -1, dtype=np.int32)
     n_unserved = 0
     for t in range(T):
+        if token_valid is not None and not token_valid[t]:
+            pair_slot[t] = -2
+            continue
         for j in range(k):
             cands = [int(c) for c in ert[ids[t, j]] if 0 <= int(c) < S]
             live = [c for c in cands if alive[c]]
@@ -193,7 +198,7 @@ def expert_ffn(x_rows: np.ndarray, w13: np.ndarray, w2: np.ndarray):
 def combine(y: np.ndarray, pair_row: np.ndarray, w: np.ndarray) -> np.ndarray:
     """out[t] = bf16(sum_j w[t, j] * y[pair_row[t, j]]) over routed pairs, rank order."""
     T, k = pair_row.shape
-    d = y.shape[1] if y.ndim == 2 and y.shape[0] else 0
+    d = y.shape[1] if y.ndim == 2 else 0
     yf = bf16_to_f64(y)
     out = np.zeros((T, d), dtype=np.float64)
     for t in range(T):
@@ -209,7 +214,7 @@ def combine(y: np.ndarray, pair_row: np.ndarray, w: np.ndarray) -> np.ndarray:
 # ----------------------------------------------------------------------------
 
 
-def route(x, wg, logits, k, ert, alive):
+def route(x, wg, logits, k, ert, alive, token_valid=None):
     """Steps 1-5: returns a dict with logits, ids, w, pair_slot, n_unserved,
     counts, offsets, perm, pair_row."""
     if logits is None:
@@ -217,16 +222,17 @@ def route(x, wg, logits, k, ert, alive):
     logits = np.asarray(logits, dtype=np.float32)
     ids = topk(logits, k)
     w = gate_weights(logits, ids)
-    pair_slot, n_unserved = remap(ids, ert, alive)
+    pair_slot, n_unserved = remap(ids, ert, alive, token_valid)
     counts, offsets, perm, pair_row = dispatch(pair_slot, alive.shape[0])
     return dict(logits=logits, ids=ids, w=w, pair_slot=pair_slot, n_unserved=n_unserved,
                 counts=counts, offsets=offsets, perm=perm, pair_row=pair_row)
 
 
-def ew_forward(x, wg, logits, k, ert, alive, w13, w2):
-    """The full EW forward on all tokens. Returns the routing dict plus
-    x_perm, h, y (bf16, in permuted row order) and out [T, d] (bf16)."""
-    r = route(x, wg, logits, k, ert, alive)
+def ew_forward(x, wg, logits, k, ert, alive, w13, w2, token_valid=None):
+    """The full EW forward on all tokens (or on the tokens marked in
+    ``token_valid``). Returns the routing dict plus x_perm, h, y (bf16, in
+    permuted row order) and out [T, d] (bf16)."""
+    r = route(x, wg, logits, k, ert, alive, token_valid)
     T, d = x.shape
     I = w13.shape[1] // 2
     P = int(r["offsets"][-1])
@@ -270,3 +276,98 @@ def ew_forward_tokens(tokens, x, wg, logits, k, ert, alive, w13_of, w2_of):
             if pair_slot[i, j] >= 0:
                 acc[i] = acc[i] + w[i, j] * bf16_to_f64(y[i, j])
     return ids, w, pair_slot, f64_to_bf16(acc)
+
+
+# ----------------------------------------------------------------------------
+# replay of failed pairs (§5.1)
+# ----------------------------------------------------------------------------
+
+
+def replay(x, k, ert, alive, w13, w2, ids, w, pair_slot, pair_row, y, out):
+    """Replays the pairs of a finished forward whose slots have since failed.
+
+    Following §5.1: a pair whose slot is no longer alive is rerouted to the
+    next live candidate of its expert (§4.2, §5.3) and recomputed there from
+    the same token row; experts are stateless and deterministic (§2.1), so
+    the recomputed output is the one the failed slot would have produced. A
+    pair that had no live candidate may now have one and is computed too. A
+    pair that loses its slot with no live candidate left is dropped (R8: the
+    other weights are not renormalised). Every token with a replayed or
+    dropped pair gets its output re-formed from its pairs' outputs in rank
+    order; other tokens keep their output.
+
+    ``ids``, ``w``, ``pair_slot``, ``pair_row``, ``y`` and ``out`` are the
+    first pass's (``ew_forward``'s) results; ``alive`` is the current mask.
+    Returns (out, replay_slot [T, k], n_replayed, n_unserved).
+    """
+    T = ids.shape[0]
+    S = alive.shape[0]
+    valid = pair_slot[:, 0] != -2 if T else np.zeros(0, bool)
+    now_slot, n_unserved = remap(ids, ert, alive, valid)
+    replay_slot = np.full((T, k), -1, dtype=np.int32)
+    changed = set()
+    for t in range(T):
+        for j in range(k):
+            prior = int(pair_slot[t, j])
+            if prior == -2 or (prior >= 0 and alive[prior]):
+                continue  # outside the batch, or the first-pass output stands
+            if now_slot[t, j] >= 0:
+                replay_slot[t, j] = now_slot[t, j]
+                changed.add(t)
+            elif prior >= 0:
+                changed.add(t)  # its slot failed and nothing can take it
+    _, offsets, perm, replay_row = dispatch(replay_slot, S)
+    n_replayed = int(offsets[-1])
+    d = x.shape[1]
+    y2 = np.zeros((n_replayed, d), dtype=np.uint16)
+    for s in range(S):
+        a, b = int(offsets[s]), int(offsets[s + 1])
+        if b > a:
+            y2[a:b] = expert_ffn(x[perm[a:b] // k], w13[s], w2[s])[1]
+    out = np.array(out, dtype=np.uint16, copy=True)
+    for t in sorted(changed):
+        acc = np.zeros(d, dtype=np.float64)
+        for j in range(k):
+            if replay_row[t, j] >= 0:
+                acc = acc + w[t, j] * bf16_to_f64(y2[replay_row[t, j]])
+            elif pair_slot[t, j] >= 0 and alive[pair_slot[t, j]]:
+                acc = acc + w[t, j] * bf16_to_f64(y[pair_row[t, j]])
+        out[t] = f64_to_bf16(acc)
+    return out, replay_slot, n_replayed, n_unserved
+
+
+# ----------------------------------------------------------------------------
+# EW-side partial batch (§5.2)
+# ----------------------------------------------------------------------------
+
+
+def batch_trigger(delivered, aw_alive, chunk_rows, T, min_rows):
+    """Which attention workers' tokens form the batch, for a fixed set of
+    delivered chunks (§5.2).
+
+    The EW starts when (0) every AW still deemed healthy has delivered, or
+    (1) the tokens buffered from healthy AWs reach the minimum batch size;
+    otherwise (2) the probing window runs out and the healthy AWs that have
+    not delivered are left out of this batch. AW a's tokens are rows
+    chunk_rows[a] .. chunk_rows[a+1]-1 of the batch buffer (clipped to
+    [0, T)). Returns (condition, token_valid [T] uint8, rows, n_aws).
+    """
+    A = len(aw_alive)
+    got = [bool(aw_alive[a]) and bool(delivered[a]) for a in range(A)]
+    spans = []
+    for a in range(A):
+        lo = min(max(int(chunk_rows[a]), 0), T)
+        hi = min(max(int(chunk_rows[a + 1]), lo), T)
+        spans.append((lo, hi))
+    rows = sum(hi - lo for (lo, hi), g in zip(spans, got) if g)
+    if all(got[a] for a in range(A) if aw_alive[a]):
+        cond = 0
+    elif rows >= min_rows:
+        cond = 1
+    else:
+        cond = 2
+    token_valid = np.zeros(T, dtype=np.uint8)
+    for (lo, hi), g in zip(spans, got):
+        if g:
+            token_valid[lo:hi] = 1
+    return cond, token_valid, rows, sum(got)

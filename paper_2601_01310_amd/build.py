@@ -24,7 +24,8 @@ COMMON = ["-O3", "-std=c++17", "-fPIC", f"-I{INCLUDE}", f"-I{CSRC}"]
 DEVICE = [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
           "-munsafe-fp-atomics"]
 
-SOURCES = ["gate_topk.hip", "dispatch.hip", "grouped_gemm.hip", "combine.hip", "tg_api.cpp"]
+SOURCES = ["gate_topk.hip", "dispatch.hip", "grouped_gemm.hip", "combine.hip", "trigger.hip",
+           "tg_api.cpp"]
 
 
 def _compile(src: str) -> str:

@@ -1,5 +1,7 @@
 // Gate-weighted combine (§2.1): out[t] = bf16(sum_j w[t,j] * y[pair_row[t,j]])
-// in float32, in rank order j = 0..k-1, skipping pairs not routed here.
+// in float32, in rank order j = 0..k-1, skipping pairs not routed here; and
+// the merge step of a replay (§5.1), which re-forms the same sum for the
+// tokens whose pairs were recomputed on another slot.
 // One block per token; each thread owns 8-element (16-byte) column chunks,
 // so the y rows are read and the output row written fully coalesced.
 #include "tg_device.h"
@@ -10,27 +12,20 @@ namespace {
 
 constexpr int kBlock = 256;
 
-__global__ __launch_bounds__(kBlock) void combine_kernel(const uint4* __restrict__ y,
-                                                         const int32_t* __restrict__ pair_row,
-                                                         const float* __restrict__ w, int T, int k,
-                                                         int nch, uint4* __restrict__ out) {
-  __shared__ int rows[32];
-  __shared__ float ws[32];
-  const int t = blockIdx.x;
-  if (threadIdx.x < k) {
-    rows[threadIdx.x] = pair_row[(size_t)t * k + threadIdx.x];
-    ws[threadIdx.x] = w[(size_t)t * k + threadIdx.x];
-  }
-  __syncthreads();
+// rows[j] >= 0: y row; rows[j] <= -2: row -rows[j]-2 of y2; -1: no output.
+__device__ __forceinline__ void combine_row(const uint4* __restrict__ y,
+                                            const uint4* __restrict__ y2, const int* rows,
+                                            const float* ws, int t, int k, int nch,
+                                            uint4* __restrict__ out) {
   for (int c = threadIdx.x; c < nch; c += kBlock) {
     float acc[8];
 #pragma unroll
     for (int i = 0; i < 8; ++i) acc[i] = 0.0f;
     for (int j = 0; j < k; ++j) {
       const int r = rows[j];
-      if (r < 0) continue;
+      if (r == -1) continue;
       const float wj = ws[j];
-      const uint4 v = y[(size_t)r * nch + c];
+      const uint4 v = (r >= 0) ? y[(size_t)r * nch + c] : y2[(size_t)(-r - 2) * nch + c];
       const uint32_t u[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
@@ -47,6 +42,55 @@ __global__ __launch_bounds__(kBlock) void combine_kernel(const uint4* __restrict
   }
 }
 
+__global__ __launch_bounds__(kBlock) void combine_kernel(const uint4* __restrict__ y,
+                                                         const int32_t* __restrict__ pair_row,
+                                                         const float* __restrict__ w, int T, int k,
+                                                         int nch, uint4* __restrict__ out) {
+  __shared__ int rows[32];
+  __shared__ float ws[32];
+  const int t = blockIdx.x;
+  if (threadIdx.x < k) {
+    const int r = pair_row[(size_t)t * k + threadIdx.x];
+    rows[threadIdx.x] = r < 0 ? -1 : r;
+    ws[threadIdx.x] = w[(size_t)t * k + threadIdx.x];
+  }
+  __syncthreads();
+  combine_row(y, nullptr, rows, ws, t, k, nch, out);
+}
+
+// One block per token; tokens whose pairs all keep their first-pass result
+// return at once.
+__global__ __launch_bounds__(kBlock) void recombine_kernel(
+    const uint4* __restrict__ y, const int32_t* __restrict__ pair_row,
+    const int32_t* __restrict__ prior, const uint8_t* __restrict__ alive, int S,
+    const uint4* __restrict__ y2, const int32_t* __restrict__ replay_row,
+    const float* __restrict__ w, int T, int k, int nch, uint4* __restrict__ out) {
+  __shared__ int rows[32];
+  __shared__ float ws[32];
+  __shared__ int changed;
+  const int t = blockIdx.x;
+  if (threadIdx.x == 0) changed = 0;
+  __syncthreads();
+  if (threadIdx.x < k) {
+    const size_t p = (size_t)t * k + threadIdx.x;
+    const int rr = replay_row[p];
+    const int ps = prior[p];
+    int r = -1;
+    if (rr >= 0) {
+      r = -rr - 2;
+      atomicOr(&changed, 1);
+    } else if (ps >= 0 && ps < S) {
+      if (alive[ps]) r = pair_row[p];
+      else atomicOr(&changed, 1);  // lost: its output leaves the sum
+    }
+    rows[threadIdx.x] = r;
+    ws[threadIdx.x] = w[p];
+  }
+  __syncthreads();
+  if (!changed) return;
+  combine_row(y, y2, rows, ws, t, k, nch, out);
+}
+
 }  // namespace
 
 hipError_t launch_combine(const uint16_t* y, const int32_t* pair_row, const float* w, int T, int k,
@@ -54,6 +98,18 @@ hipError_t launch_combine(const uint16_t* y, const int32_t* pair_row, const floa
   if (T == 0) return hipSuccess;
   hipLaunchKernelGGL(combine_kernel, dim3(T), dim3(kBlock), 0, stream,
                      reinterpret_cast<const uint4*>(y), pair_row, w, T, k, d / 8,
+                     reinterpret_cast<uint4*>(out));
+  return hipGetLastError();
+}
+
+hipError_t launch_recombine(const uint16_t* y, const int32_t* pair_row, const int32_t* prior_slot,
+                            const uint8_t* alive, int S, const uint16_t* y2,
+                            const int32_t* replay_row, const float* w, int T, int k, int d,
+                            uint16_t* out, hipStream_t stream) {
+  if (T == 0) return hipSuccess;
+  hipLaunchKernelGGL(recombine_kernel, dim3(T), dim3(kBlock), 0, stream,
+                     reinterpret_cast<const uint4*>(y), pair_row, prior_slot, alive, S,
+                     reinterpret_cast<const uint4*>(y2), replay_row, w, T, k, d / 8,
                      reinterpret_cast<uint4*>(out));
   return hipGetLastError();
 }

@@ -4,7 +4,11 @@
 // Three passes over the routed pairs, all integer and free of ordering races:
 //   1. remap_count: per pair, the first live candidate slot of its expert;
 //      per chunk of pairs, an S-wide histogram and an unserved count
-//      (integer LDS atomics: the totals do not depend on their order);
+//      (integer LDS atomics: the totals do not depend on their order).
+//      Pairs of tokens outside the batch (token_valid[t] == 0, the partial
+//      batch of §5.2) get slot -2 and are not counted. In replay mode (§5.1)
+//      a pair keeps its first-pass slot while that slot is alive and is
+//      otherwise given its first live candidate now, to be recomputed;
 //   2. scan: per-slot totals, exclusive slot offsets, and the base row of
 //      every (chunk, slot) in chunk order;
 //   3. scatter: each wave walks an equal share of a chunk in pair order and
@@ -21,10 +25,15 @@ namespace {
 constexpr int kMaxS = 1024;
 constexpr int kBlock = 256;
 
+// REPLAY: `prior` holds the first pass's slot of every pair; out_slot gets
+// the slot the pair is recomputed on, or -1 when its first-pass result still
+// stands (slot alive), it is outside the batch (-2), or no candidate is live.
+template <bool REPLAY>
 __global__ __launch_bounds__(kBlock) void remap_count_kernel(
-    const int32_t* __restrict__ ids, int npairs, const int32_t* __restrict__ ert, int E, int R,
-    const uint8_t* __restrict__ alive, int S, int32_t* __restrict__ pair_slot,
-    int32_t* __restrict__ hist, int32_t* __restrict__ unserved_chunk, int chunk) {
+    const int32_t* __restrict__ ids, int npairs, int k, const int32_t* __restrict__ ert, int E,
+    int R, const uint8_t* __restrict__ alive, int S, const uint8_t* __restrict__ token_valid,
+    const int32_t* __restrict__ prior, int32_t* __restrict__ out_slot, int32_t* __restrict__ hist,
+    int32_t* __restrict__ unserved_chunk, int chunk) {
   __shared__ int h[kMaxS];
   __shared__ int nu;
   for (int s = threadIdx.x; s < S; s += kBlock) h[s] = 0;
@@ -34,6 +43,17 @@ __global__ __launch_bounds__(kBlock) void remap_count_kernel(
   for (int i = threadIdx.x; i < chunk; i += kBlock) {
     const int p = base + i;
     if (p >= npairs) break;
+    int pr = 0;
+    if (REPLAY) {
+      pr = prior[p];
+      if (pr == -2) {
+        out_slot[p] = -1;
+        continue;
+      }
+    } else if (token_valid && !token_valid[p / k]) {
+      out_slot[p] = -2;
+      continue;
+    }
     const int e = ids[p];
     int slot = -1;
     bool listed = false;
@@ -49,11 +69,10 @@ __global__ __launch_bounds__(kBlock) void remap_count_kernel(
         }
       }
     }
-    pair_slot[p] = slot;
-    if (slot >= 0)
-      atomicAdd(&h[slot], 1);
-    else if (listed)
-      atomicAdd(&nu, 1);
+    if (slot < 0 && listed) atomicAdd(&nu, 1);
+    if (REPLAY && pr >= 0 && pr < S && alive[pr]) slot = -1;  // first-pass result stands
+    out_slot[p] = slot;
+    if (slot >= 0) atomicAdd(&h[slot], 1);
   }
   __syncthreads();
   for (int s = threadIdx.x; s < S; s += kBlock) hist[(size_t)blockIdx.x * S + s] = h[s];
@@ -65,7 +84,8 @@ __global__ __launch_bounds__(1024) void scan_kernel(int32_t* __restrict__ hist,
                                                     const int32_t* __restrict__ unserved_chunk,
                                                     int nchunks, int S, int32_t* __restrict__ counts,
                                                     int32_t* __restrict__ offsets,
-                                                    int32_t* __restrict__ n_unserved) {
+                                                    int32_t* __restrict__ n_unserved,
+                                                    int32_t* __restrict__ total_out) {
   __shared__ int sc[2][1024];
   __shared__ int nu;
   const int s = threadIdx.x;
@@ -111,7 +131,10 @@ __global__ __launch_bounds__(1024) void scan_kernel(int32_t* __restrict__ hist,
         if (c0 + i < nchunks) hist[(size_t)(c0 + i) * S + s] = v[i] + excl;
     }
   }
-  if (s == S - 1) offsets[S] = incl;
+  if (s == S - 1) {
+    offsets[S] = incl;
+    if (total_out) total_out[0] = incl;
+  }
   __syncthreads();
   if (s == 0) n_unserved[0] = nu;
 }
@@ -203,11 +226,14 @@ size_t dispatch_workspace_bytes(int T, int k, int S) {
   return ((hist + 255) & ~(size_t)255) + ((nchunks * sizeof(int32_t) + 255) & ~(size_t)255) + 256;
 }
 
-hipError_t launch_remap_dispatch(const int32_t* ids, int T, int k, const int32_t* ert, int E, int R,
-                                 const uint8_t* alive, int S, const uint16_t* x, int d,
-                                 int32_t* pair_slot, int32_t* counts, int32_t* offsets,
-                                 int32_t* perm, int32_t* pair_row, uint16_t* x_perm,
-                                 int32_t* n_unserved, void* ws, hipStream_t stream) {
+namespace {
+
+hipError_t remap_dispatch(bool replay, const int32_t* ids, int T, int k, const int32_t* ert, int E,
+                          int R, const uint8_t* alive, int S, const uint8_t* token_valid,
+                          const int32_t* prior, const uint16_t* x, int d, int32_t* pair_slot,
+                          int32_t* counts, int32_t* offsets, int32_t* perm, int32_t* pair_row,
+                          uint16_t* x_perm, int32_t* n_unserved, int32_t* total_out, void* ws,
+                          hipStream_t stream) {
   const int npairs = T * k;
   const int chunk = dispatch_chunk(npairs);
   const int nchunks = (npairs + chunk - 1) / chunk;
@@ -215,11 +241,17 @@ hipError_t launch_remap_dispatch(const int32_t* ids, int T, int k, const int32_t
   int32_t* hist = static_cast<int32_t*>(ws);
   int32_t* unserved_chunk = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + hist_bytes);
   if (nchunks > 0) {
-    hipLaunchKernelGGL(remap_count_kernel, dim3(nchunks), dim3(kBlock), 0, stream, ids, npairs, ert,
-                       E, R, alive, S, pair_slot, hist, unserved_chunk, chunk);
+    if (replay)
+      hipLaunchKernelGGL(remap_count_kernel<true>, dim3(nchunks), dim3(kBlock), 0, stream, ids,
+                         npairs, k, ert, E, R, alive, S, nullptr, prior, pair_slot, hist,
+                         unserved_chunk, chunk);
+    else
+      hipLaunchKernelGGL(remap_count_kernel<false>, dim3(nchunks), dim3(kBlock), 0, stream, ids,
+                         npairs, k, ert, E, R, alive, S, token_valid, nullptr, pair_slot, hist,
+                         unserved_chunk, chunk);
   }
   hipLaunchKernelGGL(scan_kernel, dim3(1), dim3(1024), 0, stream, hist, unserved_chunk, nchunks, S,
-                     counts, offsets, n_unserved);
+                     counts, offsets, n_unserved, total_out);
   if (nchunks > 0) {
     hipLaunchKernelGGL(scatter_kernel, dim3(nchunks), dim3(kBlock), 0, stream, pair_slot, npairs, S,
                        hist, perm, pair_row, chunk);
@@ -234,6 +266,30 @@ hipError_t launch_remap_dispatch(const int32_t* ids, int T, int k, const int32_t
     }
   }
   return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_remap_dispatch(const int32_t* ids, int T, int k, const int32_t* ert, int E, int R,
+                                 const uint8_t* alive, int S, const uint16_t* x, int d,
+                                 int32_t* pair_slot, int32_t* counts, int32_t* offsets,
+                                 int32_t* perm, int32_t* pair_row, uint16_t* x_perm,
+                                 int32_t* n_unserved, void* ws, hipStream_t stream,
+                                 const uint8_t* token_valid) {
+  return remap_dispatch(false, ids, T, k, ert, E, R, alive, S, token_valid, nullptr, x, d,
+                        pair_slot, counts, offsets, perm, pair_row, x_perm, n_unserved, nullptr,
+                        ws, stream);
+}
+
+hipError_t launch_replay_dispatch(const int32_t* ids, int T, int k, const int32_t* ert, int E,
+                                  int R, const uint8_t* alive, int S, const int32_t* prior_slot,
+                                  const uint16_t* x, int d, int32_t* replay_slot, int32_t* counts,
+                                  int32_t* offsets, int32_t* perm, int32_t* replay_row,
+                                  uint16_t* x_perm, int32_t* n_unserved, int32_t* n_replayed,
+                                  void* ws, hipStream_t stream) {
+  return remap_dispatch(true, ids, T, k, ert, E, R, alive, S, nullptr, prior_slot, x, d,
+                        replay_slot, counts, offsets, perm, replay_row, x_perm, n_unserved,
+                        n_replayed, ws, stream);
 }
 
 }  // namespace tg

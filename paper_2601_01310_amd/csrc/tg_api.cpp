@@ -33,7 +33,7 @@ tg_status hip_status(hipError_t e, const char* where) {
   return ok();
 }
 
-constexpr int kMaxK = 32, kMaxE = 1024, kMaxS = 1024, kMaxR = 16;
+constexpr int kMaxK = 32, kMaxE = 1024, kMaxS = 1024, kMaxR = 16, kMaxAws = 1024;
 
 tg_status check_gate_dims(int T, int E, int k) {
   if (T < 0) return fail(TG_ERR_BAD_DIM, "T=%d must be >= 0", T);
@@ -117,7 +117,49 @@ EwLayout ew_layout(const tg_ew_args* a, char* base) {
   const bool in_place = 2LL * a->T * a->d < (1LL << 31);
   L.x_perm = reinterpret_cast<uint16_t*>(take(in_place ? 0 : np * a->d * 2));
   L.h = reinterpret_cast<uint16_t*>(take(np * a->I * 2));
-  L.y = reinterpret_cast<uint16_t*>(take(np * a->d * 2));
+  L.y = reinterpret_cast<uint16_t*>(take(a->y ? 0 : np * a->d * 2));
+  if (a->y) L.y = a->y;
+  L.bytes = off;
+  return L;
+}
+
+// Carves the tg_ew_replay workspace; with base == nullptr only sizes it.
+struct ReplayLayout {
+  int32_t* replay_slot;
+  int32_t* counts;
+  int32_t* offsets;
+  int32_t* replay_row;
+  int32_t* perm;
+  int32_t* n_replayed;
+  int32_t* n_unserved;
+  void* dispatch_ws;
+  uint16_t* x_perm;
+  uint16_t* h;
+  uint16_t* y2;
+  size_t bytes;
+};
+
+ReplayLayout replay_layout(const tg_replay_args* a, char* base) {
+  ReplayLayout L{};
+  size_t off = 0;
+  const size_t np = (size_t)a->T * a->k;
+  auto take = [&](size_t bytes) -> char* {
+    char* p = base ? base + off : nullptr;
+    off += align256(bytes);
+    return p;
+  };
+  L.replay_slot = reinterpret_cast<int32_t*>(take(np * 4));
+  L.counts = reinterpret_cast<int32_t*>(take((size_t)a->S * 4));
+  L.offsets = reinterpret_cast<int32_t*>(take(((size_t)a->S + 1) * 4));
+  L.replay_row = reinterpret_cast<int32_t*>(take(np * 4));
+  L.perm = reinterpret_cast<int32_t*>(take(np * 4));
+  L.n_replayed = reinterpret_cast<int32_t*>(take(4));
+  L.n_unserved = reinterpret_cast<int32_t*>(take(4));
+  L.dispatch_ws = take(tg::dispatch_workspace_bytes(a->T, a->k, a->S));
+  const bool in_place = 2LL * a->T * a->d < (1LL << 31);
+  L.x_perm = reinterpret_cast<uint16_t*>(take(in_place ? 0 : np * a->d * 2));
+  L.h = reinterpret_cast<uint16_t*>(take(np * a->I * 2));
+  L.y2 = reinterpret_cast<uint16_t*>(take(np * a->d * 2));
   L.bytes = off;
   return L;
 }
@@ -271,7 +313,7 @@ static tg_status ew_forward(const tg_ew_args* a, void* ws, size_t ws_bytes, void
     e = tg::launch_remap_dispatch(ids, a->T, a->k, a->ert, a->E, a->R, a->slot_alive, a->S,
                                   in_place ? nullptr : a->x, a->d, pair_slot, counts, offsets,
                                   L.perm, pair_row, in_place ? nullptr : L.x_perm, n_unserved,
-                                  L.dispatch_ws, s);
+                                  L.dispatch_ws, s, a->token_valid);
   mark(2);
   if (e == hipSuccess)
     e = in_place ? tg::launch_ffn_gateup_gather(a->x, a->T, L.perm, a->k, offsets, a->S, max_rows,
@@ -298,6 +340,71 @@ tg_status tg_ew_forward_timed(const tg_ew_args* a, void* ws, size_t ws_bytes, vo
   for (int i = 0; i < 6; ++i)
     if (!events[i]) return fail(TG_ERR_NULL_ARG, "events[%d] is NULL", i);
   return ew_forward(a, ws, ws_bytes, stream, events);
+}
+
+static tg_status check_replay(const tg_replay_args* a) {
+  if (!a) return fail(TG_ERR_NULL_ARG, "args is NULL");
+  tg_status st = check_gate_dims(a->T, a->E, a->k);
+  if (st != TG_OK) return st;
+  if ((st = check_ffn(a->d, a->I)) != TG_OK) return st;
+  if ((st = check_slots(a->S, a->R)) != TG_OK) return st;
+  if (!a->x || !a->ert || !a->slot_alive || !a->w13 || !a->w2 || !a->topk_ids || !a->topk_w ||
+      !a->pair_slot || !a->pair_row || !a->y || !a->out)
+    return fail(TG_ERR_NULL_ARG, "a required pointer is NULL");
+  return TG_OK;
+}
+
+size_t tg_ew_replay_workspace(const tg_replay_args* a) {
+  if (check_replay(a) != TG_OK) return 0;
+  return replay_layout(a, nullptr).bytes;
+}
+
+tg_status tg_ew_replay(const tg_replay_args* a, void* ws, size_t ws_bytes, void* stream) {
+  tg_status st = check_replay(a);
+  if (st != TG_OK) return st;
+  const size_t need = replay_layout(a, nullptr).bytes;
+  if (!ws || ws_bytes < need)
+    return fail(TG_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need, ws_bytes);
+  if (reinterpret_cast<uintptr_t>(ws) & 255)
+    return fail(TG_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  ReplayLayout L = replay_layout(a, static_cast<char*>(ws));
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  int32_t* replay_slot = a->replay_slot ? a->replay_slot : L.replay_slot;
+  int32_t* n_replayed = a->n_replayed ? a->n_replayed : L.n_replayed;
+  int32_t* n_unserved = a->n_unserved ? a->n_unserved : L.n_unserved;
+  const int max_rows = a->T * a->k;
+  const bool in_place = 2LL * a->T * a->d < (1LL << 31);
+  hipError_t e = tg::launch_replay_dispatch(
+      a->topk_ids, a->T, a->k, a->ert, a->E, a->R, a->slot_alive, a->S, a->pair_slot,
+      in_place ? nullptr : a->x, a->d, replay_slot, L.counts, L.offsets, L.perm, L.replay_row,
+      in_place ? nullptr : L.x_perm, n_unserved, n_replayed, L.dispatch_ws, s);
+  if (e == hipSuccess)
+    e = in_place ? tg::launch_ffn_gateup_gather(a->x, a->T, L.perm, a->k, L.offsets, a->S,
+                                                max_rows, a->w13, a->d, a->I, L.h, s)
+                 : tg::launch_ffn_gateup(L.x_perm, L.offsets, a->S, max_rows, a->w13, a->d, a->I,
+                                         L.h, s);
+  if (e == hipSuccess)
+    e = tg::launch_ffn_down(L.h, L.offsets, a->S, max_rows, a->w2, a->d, a->I, L.y2, s);
+  if (e == hipSuccess)
+    e = tg::launch_recombine(a->y, a->pair_row, a->pair_slot, a->slot_alive, a->S, L.y2,
+                             L.replay_row, a->topk_w, a->T, a->k, a->d, a->out, s);
+  return hip_status(e, "tg_ew_replay");
+}
+
+tg_status tg_batch_trigger(const uint32_t* delivered, const uint8_t* aw_alive,
+                           const int32_t* chunk_rows, int A, int T, int min_rows,
+                           long long spin_limit, uint8_t* token_valid, int32_t* status,
+                           void* stream) {
+  if (A <= 0 || T < 0 || min_rows < 0 || spin_limit < 1)
+    return fail(TG_ERR_BAD_DIM, "A=%d > 0, T=%d >= 0, min_rows=%d >= 0, spin_limit=%lld >= 1",
+                A, T, min_rows, spin_limit);
+  if (A > kMaxAws) return fail(TG_ERR_UNSUPPORTED, "A=%d exceeds %d", A, kMaxAws);
+  if (!delivered || !aw_alive || !chunk_rows || !status || (T > 0 && !token_valid))
+    return fail(TG_ERR_NULL_ARG, "a required pointer is NULL");
+  return hip_status(tg::launch_batch_trigger(delivered, aw_alive, chunk_rows, A, T, min_rows,
+                                             spin_limit, token_valid, status,
+                                             static_cast<hipStream_t>(stream)),
+                    "tg_batch_trigger");
 }
 
 }  // extern "C"

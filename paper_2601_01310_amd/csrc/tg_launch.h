@@ -18,11 +18,25 @@ hipError_t launch_gate_topk(const uint16_t* x, const uint16_t* wg, const float* 
 constexpr int kDispatchChunks = 64;
 int dispatch_chunk(long npairs);
 size_t dispatch_workspace_bytes(int T, int k, int S);
+// token_valid (optional, [T]): pairs of tokens with 0 get pair_slot -2 and
+// are neither batched nor counted as unserved.
 hipError_t launch_remap_dispatch(const int32_t* ids, int T, int k, const int32_t* ert, int E, int R,
                                  const uint8_t* alive, int S, const uint16_t* x, int d,
                                  int32_t* pair_slot, int32_t* counts, int32_t* offsets,
                                  int32_t* perm, int32_t* pair_row, uint16_t* x_perm,
-                                 int32_t* n_unserved, void* ws, hipStream_t stream);
+                                 int32_t* n_unserved, void* ws, hipStream_t stream,
+                                 const uint8_t* token_valid = nullptr);
+// Replay batching: pairs whose first-pass slot (prior_slot) is no longer
+// alive, or that had no live candidate, go to their first live candidate now
+// (replay_slot; -1 for every other pair) and are batched by (slot, token,
+// rank) into rows replay_row; n_replayed = number of such rows. Same
+// workspace as launch_remap_dispatch.
+hipError_t launch_replay_dispatch(const int32_t* ids, int T, int k, const int32_t* ert, int E,
+                                  int R, const uint8_t* alive, int S, const int32_t* prior_slot,
+                                  const uint16_t* x, int d, int32_t* replay_slot, int32_t* counts,
+                                  int32_t* offsets, int32_t* perm, int32_t* replay_row,
+                                  uint16_t* x_perm, int32_t* n_unserved, int32_t* n_replayed,
+                                  void* ws, hipStream_t stream);
 
 hipError_t launch_ffn_gateup(const uint16_t* x_perm, const int32_t* offsets, int S, int max_rows,
                              const uint16_t* w13, int d, int I, uint16_t* h, hipStream_t stream);
@@ -40,5 +54,23 @@ hipError_t launch_expert_ffn(const uint16_t* x_perm, const int32_t* offsets, int
 
 hipError_t launch_combine(const uint16_t* y, const int32_t* pair_row, const float* w, int T, int k,
                           int d, uint16_t* out, hipStream_t stream);
+// Re-forms out[t] for every token with a replayed pair or a pair whose
+// first-pass slot has failed with no live candidate left; other rows of out
+// are left as they are. A pair's output comes from y2[replay_row] when it was
+// replayed, from y[pair_row] when its first-pass slot is still alive, and is
+// absent otherwise. Same float32 rank-order sum as launch_combine.
+hipError_t launch_recombine(const uint16_t* y, const int32_t* pair_row, const int32_t* prior_slot,
+                            const uint8_t* alive, int S, const uint16_t* y2,
+                            const int32_t* replay_row, const float* w, int T, int k, int d,
+                            uint16_t* out, hipStream_t stream);
+
+// Partial-batch trigger (one block): waits until every live AW has
+// delivered, or the delivered rows of live AWs reach min_rows, or spin_limit
+// polls have passed; then marks the rows of the delivered live AWs in
+// token_valid [T] and writes status [4].
+hipError_t launch_batch_trigger(const uint32_t* delivered, const uint8_t* aw_alive,
+                                const int32_t* chunk_rows, int A, int T, int min_rows,
+                                long long spin_limit, uint8_t* token_valid, int32_t* status,
+                                hipStream_t stream);
 
 }  // namespace tg

@@ -21,7 +21,8 @@ TG_OK, TG_ERR_NULL_ARG, TG_ERR_BAD_DIM, TG_ERR_UNSUPPORTED, TG_ERR_WORKSPACE, TG
 EXPORTS = [
     "tg_status_string", "tg_last_error", "tg_gate_topk", "tg_remap_dispatch_workspace",
     "tg_remap_dispatch", "tg_expert_ffn_grouped", "tg_combine", "tg_ew_forward_workspace",
-    "tg_ew_forward", "tg_ew_forward_timed",
+    "tg_ew_forward", "tg_ew_forward_timed", "tg_ew_replay_workspace", "tg_ew_replay",
+    "tg_batch_trigger",
 ]
 
 
@@ -39,7 +40,17 @@ class EwArgs(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int) for n in ("T", "d", "E", "k", "I", "S", "R")] + [
         (n, ctypes.c_void_p) for n in (
             "x", "w_gate", "logits_in", "ert", "slot_alive", "w13", "w2", "out", "topk_ids",
-            "topk_w", "pair_slot", "slot_counts", "slot_offsets", "pair_row", "n_unserved")
+            "topk_w", "pair_slot", "slot_counts", "slot_offsets", "pair_row", "n_unserved", "y",
+            "token_valid")
+    ]
+
+
+class ReplayArgs(ctypes.Structure):
+    """Mirror of ``tg_replay_args``."""
+    _fields_ = [(n, ctypes.c_int) for n in ("T", "d", "E", "k", "I", "S", "R")] + [
+        (n, ctypes.c_void_p) for n in (
+            "x", "ert", "slot_alive", "w13", "w2", "topk_ids", "topk_w", "pair_slot", "pair_row",
+            "y", "out", "replay_slot", "n_replayed", "n_unserved")
     ]
 
 
@@ -75,6 +86,12 @@ def load(path: Optional[str] = None):
     lib.tg_ew_forward_timed.restype = i
     lib.tg_ew_forward_timed.argtypes = [ctypes.POINTER(EwArgs), vp, sz, vp,
                                         ctypes.POINTER(ctypes.c_void_p), i]
+    lib.tg_ew_replay_workspace.restype = sz
+    lib.tg_ew_replay_workspace.argtypes = [ctypes.POINTER(ReplayArgs)]
+    lib.tg_ew_replay.restype = i
+    lib.tg_ew_replay.argtypes = [ctypes.POINTER(ReplayArgs), vp, sz, vp]
+    lib.tg_batch_trigger.restype = i
+    lib.tg_batch_trigger.argtypes = [vp, vp, vp, i, i, i, ctypes.c_longlong, vp, vp, vp]
     _lib = lib
     return lib
 
@@ -135,13 +152,27 @@ def tg_combine(y, pair_row, topk_w, T, k, d, out, stream=None):
 
 def make_ew_args(T, d, E, k, I, S, R, x, w_gate, logits_in, ert, slot_alive, w13, w2, out,
                  topk_ids=None, topk_w=None, pair_slot=None, slot_counts=None, slot_offsets=None,
-                 pair_row=None, n_unserved=None) -> EwArgs:
+                 pair_row=None, n_unserved=None, y=None, token_valid=None) -> EwArgs:
     a = EwArgs()
     a.T, a.d, a.E, a.k, a.I, a.S, a.R = T, d, E, k, I, S, R
     for name, v in dict(x=x, w_gate=w_gate, logits_in=logits_in, ert=ert, slot_alive=slot_alive,
                         w13=w13, w2=w2, out=out, topk_ids=topk_ids, topk_w=topk_w,
                         pair_slot=pair_slot, slot_counts=slot_counts, slot_offsets=slot_offsets,
-                        pair_row=pair_row, n_unserved=n_unserved).items():
+                        pair_row=pair_row, n_unserved=n_unserved, y=y,
+                        token_valid=token_valid).items():
+        setattr(a, name, _p(v))
+    return a
+
+
+def make_replay_args(T, d, E, k, I, S, R, x, ert, slot_alive, w13, w2, topk_ids, topk_w,
+                     pair_slot, pair_row, y, out, replay_slot=None, n_replayed=None,
+                     n_unserved=None) -> ReplayArgs:
+    a = ReplayArgs()
+    a.T, a.d, a.E, a.k, a.I, a.S, a.R = T, d, E, k, I, S, R
+    for name, v in dict(x=x, ert=ert, slot_alive=slot_alive, w13=w13, w2=w2, topk_ids=topk_ids,
+                        topk_w=topk_w, pair_slot=pair_slot, pair_row=pair_row, y=y, out=out,
+                        replay_slot=replay_slot, n_replayed=n_replayed,
+                        n_unserved=n_unserved).items():
         setattr(a, name, _p(v))
     return a
 
@@ -162,6 +193,32 @@ def tg_ew_forward_timed(args: EwArgs, ws, ws_bytes, events, stream=None):
                                       len(events)), "tg_ew_forward_timed")
 
 
+def tg_batch_trigger(delivered, aw_alive, chunk_rows, A, T, min_rows, spin_limit, token_valid,
+                     status, stream=None):
+    """``delivered`` may be a device tensor or a pinned host tensor (its
+    device-visible address is passed)."""
+    _check(load().tg_batch_trigger(_flag_ptr(delivered), _p(aw_alive), _p(chunk_rows), A, T,
+                                   min_rows, spin_limit, _p(token_valid), _p(status),
+                                   _stream(stream)), "tg_batch_trigger")
+
+
+def _flag_ptr(t):
+    if isinstance(t, torch.Tensor) and t.device.type == "cpu":
+        if not t.is_pinned() or not t.is_contiguous():
+            raise ValueError("host flags must be a contiguous pinned tensor")
+        return t.data_ptr()  # pinned host memory is mapped at the same address on the device
+    return _p(t)
+
+
+def tg_ew_replay_workspace(args: ReplayArgs) -> int:
+    return int(load().tg_ew_replay_workspace(ctypes.byref(args)))
+
+
+def tg_ew_replay(args: ReplayArgs, ws, ws_bytes, stream=None):
+    _check(load().tg_ew_replay(ctypes.byref(args), _p(ws), ws_bytes, _stream(stream)),
+           "tg_ew_replay")
+
+
 # ----------------------------------------------------------------------------
 # Convenience wrappers: allocate outputs with torch, then call the C ABI.
 # ----------------------------------------------------------------------------
@@ -174,9 +231,13 @@ def workspace(nbytes: int, device) -> torch.Tensor:
 
 class EwForward:
     """Holds the outputs and workspace of one workload shape so repeated calls
-    allocate nothing (the timed loop of the benchmark reuses one of these)."""
+    allocate nothing (the timed loop of the benchmark reuses one of these).
 
-    def __init__(self, wl, alive=None):
+    ``keep_y`` keeps the per-pair expert outputs in ``self.y`` so that failed
+    pairs can be replayed afterwards (``replay``); ``token_valid`` ([T] uint8)
+    restricts the batch to the tokens marked 1."""
+
+    def __init__(self, wl, alive=None, keep_y=False, token_valid=None):
         dev = wl.x.device
         T, k, S = wl.T, wl.k, wl.S
         self.wl = wl
@@ -189,14 +250,18 @@ class EwForward:
         self.slot_offsets = torch.empty((S + 1,), dtype=torch.int32, device=dev)
         self.pair_row = torch.empty((T, k), dtype=torch.int32, device=dev)
         self.n_unserved = torch.empty((1,), dtype=torch.int32, device=dev)
+        self.y = (torch.empty((max(T * k, 1), wl.d), dtype=torch.bfloat16, device=dev)
+                  if keep_y else None)
+        self.token_valid = token_valid
         self.args = make_ew_args(
             T, wl.d, wl.E, k, wl.I, S, wl.R, wl.x, wl.wg, wl.logits, wl.ert, self.alive, wl.w13,
             wl.w2, self.out, self.topk_ids, self.topk_w, self.pair_slot, self.slot_counts,
-            self.slot_offsets, self.pair_row, self.n_unserved)
+            self.slot_offsets, self.pair_row, self.n_unserved, self.y, token_valid)
         self.ws_bytes = tg_ew_forward_workspace(self.args)
         if self.ws_bytes == 0:
             raise TgError(load().tg_ew_forward(ctypes.byref(self.args), None, 0, None), "workspace")
         self.ws = workspace(self.ws_bytes, dev)
+        self._replay = None
 
     def __call__(self, stream=None):
         tg_ew_forward(self.args, self.ws, self.ws_bytes, stream)
@@ -205,3 +270,27 @@ class EwForward:
     def set_alive(self, alive):
         self.alive = alive
         self.args.slot_alive = _p(alive)
+
+    def replay(self, alive, stream=None):
+        """Replays the pairs of the last forward whose slots are not alive in
+        ``alive`` (needs ``keep_y``); updates ``self.out`` in place and
+        returns (replay_slot, n_replayed, n_unserved) device tensors."""
+        if self.y is None:
+            raise ValueError("construct EwForward with keep_y=True to replay")
+        wl, dev = self.wl, self.out.device
+        if self._replay is None:
+            r = dict(replay_slot=torch.empty((wl.T, wl.k), dtype=torch.int32, device=dev),
+                     n_replayed=torch.empty((1,), dtype=torch.int32, device=dev),
+                     n_unserved=torch.empty((1,), dtype=torch.int32, device=dev))
+            r["args"] = make_replay_args(
+                wl.T, wl.d, wl.E, wl.k, wl.I, wl.S, wl.R, wl.x, wl.ert, alive, wl.w13, wl.w2,
+                self.topk_ids, self.topk_w, self.pair_slot, self.pair_row, self.y, self.out,
+                r["replay_slot"], r["n_replayed"], r["n_unserved"])
+            r["ws_bytes"] = tg_ew_replay_workspace(r["args"])
+            r["ws"] = workspace(r["ws_bytes"], dev)
+            self._replay = r
+        r = self._replay
+        r["alive"] = alive
+        r["args"].slot_alive = _p(alive)
+        tg_ew_replay(r["args"], r["ws"], r["ws_bytes"], stream)
+        return r["replay_slot"], r["n_replayed"], r["n_unserved"]

@@ -141,6 +141,53 @@ def test_ew_forward_rejects_bad_arguments(lib):
     assert lib.tg_ew_forward(None, P, need, None) == tg.TG_ERR_NULL_ARG
 
 
+def test_ew_replay_rejects_bad_arguments(lib):
+    a = tg.ReplayArgs()
+    a.T, a.d, a.E, a.k, a.I, a.S, a.R = 8, 256, 8, 2, 512, 10, 2
+    for n in ("x", "ert", "slot_alive", "w13", "w2", "topk_ids", "topk_w", "pair_slot",
+              "pair_row", "y", "out"):
+        setattr(a, n, P)
+    need = lib.tg_ew_replay_workspace(ctypes.byref(a))
+    assert need > 0
+    assert lib.tg_ew_replay(ctypes.byref(a), P, need - 1, None) == tg.TG_ERR_WORKSPACE
+    assert lib.tg_ew_replay(ctypes.byref(a), P + 16, need, None) == tg.TG_ERR_WORKSPACE
+    a.y = None  # the first pass's per-pair outputs are required
+    assert lib.tg_ew_replay(ctypes.byref(a), P, need, None) == tg.TG_ERR_NULL_ARG
+    assert lib.tg_ew_replay_workspace(ctypes.byref(a)) == 0
+    a.y = P
+    a.k = 9
+    assert lib.tg_ew_replay(ctypes.byref(a), P, need, None) == tg.TG_ERR_BAD_DIM
+    a.k, a.I = 2, 100
+    assert lib.tg_ew_replay(ctypes.byref(a), P, need, None) == tg.TG_ERR_UNSUPPORTED
+    assert lib.tg_ew_replay(None, P, need, None) == tg.TG_ERR_NULL_ARG
+
+
+def test_kept_outputs_shrink_the_forward_workspace(lib):
+    a = tg.EwArgs()
+    a.T, a.d, a.E, a.k, a.I, a.S, a.R = 64, 256, 8, 2, 512, 10, 2
+    for n in ("x", "w_gate", "ert", "slot_alive", "w13", "w2", "out"):
+        setattr(a, n, P)
+    need = lib.tg_ew_forward_workspace(ctypes.byref(a))
+    a.y = P  # per-pair outputs in a caller buffer instead of the workspace
+    assert lib.tg_ew_forward_workspace(ctypes.byref(a)) == need - 64 * 2 * 256 * 2
+
+
+def test_batch_trigger_rejects_bad_arguments(lib):
+    def call(**kw):
+        a = dict(d=P, al=P, cr=P, A=4, T=64, m=16, spin=10, tv=P, st=P)
+        a.update(kw)
+        return lib.tg_batch_trigger(a["d"], a["al"], a["cr"], a["A"], a["T"], a["m"], a["spin"],
+                                    a["tv"], a["st"], None)
+    assert call(A=0) == tg.TG_ERR_BAD_DIM
+    assert call(T=-1) == tg.TG_ERR_BAD_DIM
+    assert call(m=-1) == tg.TG_ERR_BAD_DIM
+    assert call(spin=0) == tg.TG_ERR_BAD_DIM
+    assert call(A=1025) == tg.TG_ERR_UNSUPPORTED
+    assert call(d=None) == tg.TG_ERR_NULL_ARG
+    assert call(tv=None) == tg.TG_ERR_NULL_ARG
+    assert call(st=None) == tg.TG_ERR_NULL_ARG
+
+
 def test_binding_refuses_host_tensors(lib):
     import torch
     with pytest.raises(ValueError):

@@ -359,6 +359,131 @@ def test_unserved_pairs_are_dropped_without_renormalising(tiny):
     assert np.array_equal(r1["out"][t], want)
 
 
+# ---------------------------------------------------------------- partial batch (§5.2)
+
+
+def test_partial_batch_equals_forward_on_the_included_tokens(tiny):
+    """Tokens outside the batch are not routed (pair_slot -2) and get +0; the
+    other tokens get exactly what a forward over them alone gives."""
+    a = _np_workload(tiny)
+    valid = np.random.default_rng(3).random(tiny.T) < 0.6
+    a["alive"] = a["alive"].copy()
+    a["alive"][1] = 0  # expert 1 unserved: only included tokens may count
+    r = O.ew_forward(**a, token_valid=valid)
+    rs = O.ew_forward(**dict(a, x=a["x"][valid]))
+    assert np.array_equal(r["out"][valid], rs["out"])
+    assert not r["out"][~valid].any()
+    assert (r["pair_slot"][~valid] == -2).all() and (r["pair_row"][~valid] == -1).all()
+    assert np.array_equal(r["pair_slot"][valid], rs["pair_slot"])
+    assert r["n_unserved"] == rs["n_unserved"] == int((rs["ids"] == 1).sum()) > 0
+    assert np.array_equal(r["counts"], rs["counts"])
+
+
+def test_batch_trigger_brute_force_over_delivery_and_liveness():
+    """Every combination of delivered / healthy flags over 4 AWs (one with an
+    empty chunk, one partly past T): the batch is exactly the rows of healthy
+    AWs that delivered, and the condition follows the rule of §5.2."""
+    chunk_rows = [0, 10, 25, 25, 60]
+    T = 48
+    rows_of = [10, 15, 0, 23]
+    for bits in itertools.product([0, 1], repeat=8):
+        delivered, alive = bits[:4], bits[4:]
+        for min_rows in (0, 20, 49):
+            cond, tv, rows, n = O.batch_trigger(delivered, alive, chunk_rows, T, min_rows)
+            inc = [a for a in range(4) if delivered[a] and alive[a]]
+            want = np.zeros(T, dtype=np.uint8)
+            for a in inc:
+                want[chunk_rows[a]:min(chunk_rows[a + 1], T)] = 1
+            assert np.array_equal(tv, want) and rows == int(want.sum()) == sum(rows_of[a] for a in inc)
+            assert n == len(inc)
+            everyone = all(delivered[a] for a in range(4) if alive[a])
+            assert cond == (0 if everyone else 1 if rows >= min_rows else 2)
+
+
+# ---------------------------------------------------------------- replay (§5.1)
+
+
+def _replay(tiny, a, r0, alive, y=None, out=None):
+    return O.replay(a["x"], tiny.k, a["ert"], alive, a["w13"], a["w2"], r0["ids"], r0["w"],
+                    r0["pair_slot"], r0["pair_row"], r0["y"] if y is None else y,
+                    r0["out"] if out is None else out)
+
+
+def _lost_outputs(r, slot):
+    """Outputs of ``slot`` that never arrived: its y rows and the out rows of
+    its tokens hold NaN."""
+    y, out = r["y"].copy(), r["out"].copy()
+    hit = r["pair_slot"] == slot
+    y[r["pair_row"][hit]] = 0x7FC0
+    out[np.flatnonzero(hit.any(axis=1))] = 0x7FC0
+    return y, out
+
+
+def test_replay_after_a_mid_layer_failure_equals_the_failover_forward(tiny):
+    """Slot 3 fails after the first pass: its pairs are recomputed on the
+    shadow (slot 9) and the result equals a forward that routed them there
+    from the start."""
+    a = _np_workload(tiny)
+    r0 = O.ew_forward(**a)
+    alive1 = host(tiny.alive_after_failure())
+    r1 = O.ew_forward(**dict(a, alive=alive1))
+    y, out = _lost_outputs(r0, 3)
+    out2, rs, n_rep, n_un = _replay(tiny, a, r0, alive1, y, out)
+    assert np.array_equal(out2, r1["out"])
+    assert np.array_equal(rs >= 0, r0["pair_slot"] == 3) and (rs[rs >= 0] == 9).all()
+    assert n_rep == int((r0["pair_slot"] == 3).sum()) > 0
+    assert n_un == r1["n_unserved"] == 0
+
+
+def test_replay_with_nothing_failed_changes_nothing(tiny):
+    a = _np_workload(tiny)
+    r0 = O.ew_forward(**a)
+    out2, rs, n_rep, n_un = _replay(tiny, a, r0, a["alive"])
+    assert np.array_equal(out2, r0["out"]) and (rs == -1).all() and n_rep == 0 and n_un == 0
+
+
+def test_replay_drops_pairs_whose_expert_has_no_live_candidate(tiny):
+    """Slot 1 (expert 1, no shadow) fails: its pairs leave the sums, the
+    other weights are not renormalised, as in a forward without slot 1."""
+    a = _np_workload(tiny)
+    r0 = O.ew_forward(**a)
+    alive1 = a["alive"].copy()
+    alive1[1] = 0
+    r1 = O.ew_forward(**dict(a, alive=alive1))
+    out2, rs, n_rep, n_un = _replay(tiny, a, r0, alive1)
+    assert np.array_equal(out2, r1["out"])
+    assert n_rep == 0 and (rs == -1).all()
+    assert n_un == r1["n_unserved"] == int((r0["ids"] == 1).sum()) > 0
+    untouched = ~(r0["pair_slot"] == 1).any(axis=1)
+    assert np.array_equal(out2[untouched], r0["out"][untouched])
+
+
+def test_replay_computes_pairs_that_had_no_live_candidate(tiny):
+    """Expert 3 was unserved (slots 3 and 9 dead); once slot 3 is back its
+    pairs are computed and merged."""
+    a = _np_workload(tiny)
+    alive0 = a["alive"].copy()
+    alive0[[3, 9]] = 0
+    r0 = O.ew_forward(**dict(a, alive=alive0))
+    r1 = O.ew_forward(**a)
+    out2, rs, n_rep, n_un = _replay(tiny, a, r0, a["alive"])
+    assert np.array_equal(out2, r1["out"])
+    assert np.array_equal(rs >= 0, r0["ids"] == 3) and (rs[rs >= 0] == 3).all()
+    assert n_rep == r0["n_unserved"] > 0 and n_un == 0
+
+
+def test_replay_leaves_tokens_outside_the_batch_alone(tiny):
+    a = _np_workload(tiny)
+    valid = np.random.default_rng(5).random(tiny.T) < 0.5
+    r0 = O.ew_forward(**a, token_valid=valid)
+    alive1 = host(tiny.alive_after_failure())
+    r1 = O.ew_forward(**dict(a, alive=alive1), token_valid=valid)
+    y, out = _lost_outputs(r0, 3)
+    out2, rs, n_rep, _ = _replay(tiny, a, r0, alive1, y, out)
+    assert np.array_equal(out2, r1["out"]) and not out2[~valid].any()
+    assert (rs[~valid] == -1).all() and n_rep == int((r0["pair_slot"] == 3).sum())
+
+
 def test_partial_combines_over_expert_shares_add_up():
     """Each EW of an expert-parallel group sums only its local pairs with the
     global weights; summing the partials of all shares gives the full MoE
