@@ -273,6 +273,63 @@ def replay_cost(wl, steps, warmup):
     return res
 
 
+def partial_batch_cost(wl, steps, warmup, n_aws=8, late=(3,)):
+    """EW-side partial batch (§5.2): the workload's tokens arrive from n_aws
+    attention workers in equal chunks; the AWs in ``late`` never deliver and
+    the trigger fires on the minimum batch (the other AWs' rows). Times the
+    trigger alone, trigger + forward on the partial batch, and the forward
+    on the full batch (HIP events, p50)."""
+    import torch
+    from ctypes import c_void_p
+
+    from paper_2601_01310_amd import tg
+
+    dev = wl.x.device
+    hip = HipEvents()
+    stream = torch.cuda.current_stream()
+    bounds = [wl.T * a // n_aws for a in range(n_aws + 1)]
+    chunk_rows = torch.tensor(bounds, dtype=torch.int32, device=dev)
+    delivered = torch.tensor([0 if a in late else 1 for a in range(n_aws)], dtype=torch.int32,
+                             device=dev)
+    alive = torch.ones(n_aws, dtype=torch.uint8, device=dev)
+    min_rows = sum(bounds[a + 1] - bounds[a] for a in range(n_aws) if a not in late)
+    tv = torch.empty(wl.T, dtype=torch.uint8, device=dev)
+    st = torch.empty(4, dtype=torch.int32, device=dev)
+    part = tg.EwForward(wl, token_valid=tv)
+    full = tg.EwForward(wl)
+
+    def trigger():
+        tg.tg_batch_trigger(delivered, alive, chunk_rows, n_aws, wl.T, min_rows, 1000, tv, st,
+                            stream)
+
+    def both():
+        trigger()
+        part(stream)
+
+    def timed(fn):
+        for _ in range(warmup):
+            fn()
+        ev = hip.create(2 * steps)
+        torch.cuda.synchronize()
+        for i in range(steps):
+            hip.hip.hipEventRecord(c_void_p(ev[2 * i]), c_void_p(stream.cuda_stream))
+            fn()
+            hip.hip.hipEventRecord(c_void_p(ev[2 * i + 1]), c_void_p(stream.cuda_stream))
+        torch.cuda.synchronize()
+        us = sorted(hip.elapsed_ms(ev[2 * i], ev[2 * i + 1]) * 1e3 for i in range(steps))
+        hip.destroy(ev)
+        return us[len(us) // 2]
+
+    res = {"workload": wl.name, "aws": n_aws, "late_aws": list(late),
+           "trigger_us_p50": timed(trigger), "trigger_plus_partial_forward_us_p50": timed(both),
+           "full_forward_us_p50": timed(lambda: full(stream))}
+    s = st.cpu().tolist()
+    res.update({"condition": s[0], "rows_in_batch": s[1], "aws_in_batch": s[2],
+                "pairs_partial": int(part.slot_offsets[-1]), "pairs_full": int(full.slot_offsets[-1])})
+    print(json.dumps(res), flush=True)
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -287,6 +344,8 @@ def main():
                          "point instead of the benchmark line)")
     ap.add_argument("--shadow", action="store_true",
                     help="idle-shadow / concurrent-expert interference check (one JSON line)")
+    ap.add_argument("--partial", action="store_true",
+                    help="partial-batch trigger + forward against the full forward (one JSON line)")
     ap.add_argument("--replay", action="store_true",
                     help="cost of replaying the failed primaries' pairs after a forward, against "
                          "the forward (one JSON line)")
@@ -322,6 +381,9 @@ def main():
     wl = synth.make(args.workload, device=dev)
     if args.replay:
         replay_cost(wl, args.steps, args.warmup)
+        return
+    if args.partial:
+        partial_batch_cost(wl, args.steps, args.warmup)
         return
     alive = wl.alive_after_failure() if args.failover else wl.alive
     f = tg.EwForward(wl, alive)

@@ -30,6 +30,15 @@ What is computed, per token t of one MoE layer (§2.1; §4.2; §5.1; §5.3):
    of w * y), +0 when the token has no routed pair here (gate-weighted sum,
    §2.1).
 
+Beyond the single forward (§5.1, §5.2):
+
+8. partial batch  tokens outside the batch (their attention worker has not
+   delivered, §5.2) are not routed and get +0; ``batch_trigger`` decides
+   which workers' tokens form the batch;
+9. replay         after a forward, pairs whose slot has failed are rerouted
+   to the next live candidate, recomputed from the same token row and merged
+   into the output (§5.1).
+
 Readings where the paper is silent (each listed in the design notes): the
 SwiGLU form and layouts, the bf16 rounding points of h, y and out, the
 tie-break, the permutation order, first-alive replica choice, partial combine
