@@ -13,6 +13,8 @@
 //      every (chunk, slot) in chunk order;
 //   3. scatter: each wave walks an equal share of a chunk in pair order and
 //      ranks equal slots with ballots, so rows follow (slot, token, rank).
+// Up to 2048 pairs, one block runs all three passes (the batch of a decode
+// step fits, and two launches are saved).
 // The gather then copies one activation row per routed pair with 16-byte
 // loads and stores (rows are contiguous in source and destination, so the
 // copy is fully coalesced without staging).
@@ -24,6 +26,45 @@ namespace {
 
 constexpr int kMaxS = 1024;
 constexpr int kBlock = 256;
+
+// Slot that pair p is computed on: the first live ERT candidate of its
+// expert; -2 for a token outside the batch. REPLAY: -1 also when the first
+// pass's slot prior[p] is still alive (its result stands) or the token was
+// outside the batch. *unserved: the expert lists a local candidate, none
+// alive.
+template <bool REPLAY>
+__device__ __forceinline__ int resolve_pair(int p, const int32_t* __restrict__ ids, int k,
+                                            const int32_t* __restrict__ ert, int E, int R,
+                                            const uint8_t* __restrict__ alive, int S,
+                                            const uint8_t* __restrict__ token_valid,
+                                            const int32_t* __restrict__ prior, bool* unserved) {
+  *unserved = false;
+  int pr = 0;
+  if (REPLAY) {
+    pr = prior[p];
+    if (pr == -2) return -1;
+  } else if (token_valid && !token_valid[p / k]) {
+    return -2;
+  }
+  const int e = ids[p];
+  int slot = -1;
+  bool listed = false;
+  if (e >= 0 && e < E) {
+    for (int r = 0; r < R; ++r) {
+      const int c = ert[(size_t)e * R + r];
+      if (c >= 0 && c < S) {
+        listed = true;
+        if (alive[c]) {
+          slot = c;
+          break;
+        }
+      }
+    }
+  }
+  *unserved = slot < 0 && listed;
+  if (REPLAY && pr >= 0 && pr < S && alive[pr]) slot = -1;  // first-pass result stands
+  return slot;
+}
 
 // REPLAY: `prior` holds the first pass's slot of every pair; out_slot gets
 // the slot the pair is recomputed on, or -1 when its first-pass result still
@@ -43,35 +84,11 @@ __global__ __launch_bounds__(kBlock) void remap_count_kernel(
   for (int i = threadIdx.x; i < chunk; i += kBlock) {
     const int p = base + i;
     if (p >= npairs) break;
-    int pr = 0;
-    if (REPLAY) {
-      pr = prior[p];
-      if (pr == -2) {
-        out_slot[p] = -1;
-        continue;
-      }
-    } else if (token_valid && !token_valid[p / k]) {
-      out_slot[p] = -2;
-      continue;
-    }
-    const int e = ids[p];
-    int slot = -1;
-    bool listed = false;
-    if (e >= 0 && e < E) {
-      for (int r = 0; r < R; ++r) {
-        const int c = ert[(size_t)e * R + r];
-        if (c >= 0 && c < S) {
-          listed = true;
-          if (alive[c]) {
-            slot = c;
-            break;
-          }
-        }
-      }
-    }
-    if (slot < 0 && listed) atomicAdd(&nu, 1);
-    if (REPLAY && pr >= 0 && pr < S && alive[pr]) slot = -1;  // first-pass result stands
+    bool unserved;
+    const int slot =
+        resolve_pair<REPLAY>(p, ids, k, ert, E, R, alive, S, token_valid, prior, &unserved);
     out_slot[p] = slot;
+    if (unserved) atomicAdd(&nu, 1);
     if (slot >= 0) atomicAdd(&h[slot], 1);
   }
   __syncthreads();
@@ -196,6 +213,106 @@ __global__ __launch_bounds__(kBlock) void scatter_kernel(const int32_t* __restri
   }
 }
 
+// All three passes in one block of 1024 threads, for at most kSmallPairs
+// pairs: thread i resolves pairs i, i + 1024, ...; a block-wide scan gives
+// the offsets; then the pairs are ranked 1024 at a time in pair order (wave
+// w holds pairs 64w .. 64w+63 of the group) exactly as scatter_kernel does,
+// so rows follow (slot, token, rank).
+constexpr int kOneBlock = 1024;
+constexpr int kSmallPairs = 2048;
+constexpr int kSmallPer = kSmallPairs / kOneBlock;
+
+template <bool REPLAY>
+__global__ __launch_bounds__(kOneBlock) void dispatch_one_block_kernel(
+    const int32_t* __restrict__ ids, int npairs, int k, const int32_t* __restrict__ ert, int E,
+    int R, const uint8_t* __restrict__ alive, int S, const uint8_t* __restrict__ token_valid,
+    const int32_t* __restrict__ prior, int32_t* __restrict__ out_slot, int32_t* __restrict__ counts,
+    int32_t* __restrict__ offsets, int32_t* __restrict__ perm, int32_t* __restrict__ pair_row,
+    int32_t* __restrict__ n_unserved, int32_t* __restrict__ total_out) {
+  constexpr int kWaves = kOneBlock / kWave;
+  __shared__ int cnt[kWaves][kMaxS];
+  __shared__ int run[kMaxS];
+  __shared__ int sc[2][kOneBlock];
+  __shared__ int nu;
+  const int tid = threadIdx.x;
+  const int wave = tid / kWave, lane = lane_id();
+  for (int s = tid; s < S; s += kOneBlock) run[s] = 0;
+  if (tid == 0) nu = 0;
+  __syncthreads();
+  int my_slot[kSmallPer];
+#pragma unroll
+  for (int i = 0; i < kSmallPer; ++i) {
+    const int p = tid + i * kOneBlock;
+    my_slot[i] = -1;
+    if (p < npairs) {
+      bool unserved;
+      my_slot[i] =
+          resolve_pair<REPLAY>(p, ids, k, ert, E, R, alive, S, token_valid, prior, &unserved);
+      out_slot[p] = my_slot[i];
+      if (unserved) atomicAdd(&nu, 1);
+      if (my_slot[i] >= 0) atomicAdd(&run[my_slot[i]], 1);
+    }
+  }
+  __syncthreads();
+  // Exclusive scan of the slot totals (Hillis-Steele over 1024 entries).
+  const int total = (tid < S) ? run[tid] : 0;
+  sc[0][tid] = total;
+  __syncthreads();
+  int cur = 0;
+  for (int off = 1; off < kOneBlock; off <<= 1) {
+    sc[cur ^ 1][tid] = sc[cur][tid] + (tid >= off ? sc[cur][tid - off] : 0);
+    cur ^= 1;
+    __syncthreads();
+  }
+  const int incl = sc[cur][tid];
+  if (tid < S) {
+    counts[tid] = total;
+    offsets[tid] = incl - total;
+    run[tid] = incl - total;
+  }
+  if (tid == S - 1) {
+    offsets[S] = incl;
+    if (total_out) total_out[0] = incl;
+  }
+  if (tid == 0) n_unserved[0] = nu;
+  const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+#pragma unroll
+  for (int i = 0; i < kSmallPer; ++i) {
+    if (i * kOneBlock >= npairs) break;  // uniform
+    for (int j = tid; j < kWaves * S; j += kOneBlock) cnt[j / S][j % S] = 0;
+    __syncthreads();
+    const int s = my_slot[i];
+    if (s >= 0) atomicAdd(&cnt[wave][s], 1);
+    __syncthreads();
+    for (int q = tid; q < S; q += kOneBlock) {
+      int r = run[q];
+      for (int w = 0; w < kWaves; ++w) {
+        const int v = cnt[w][q];
+        cnt[w][q] = r;
+        r += v;
+      }
+      run[q] = r;
+    }
+    __syncthreads();
+    const int p = tid + i * kOneBlock;
+    if (p < npairs && s < 0) pair_row[p] = -1;
+    uint64_t active = __ballot(s >= 0);
+    while (active) {
+      const int leader = __builtin_ctzll(active);
+      const int sl = __shfl(s, leader);
+      const uint64_t m = __ballot(s == sl) & active;
+      if (s == sl) {
+        const int row = cnt[wave][sl] + __builtin_popcountll(m & lt);
+        perm[row] = p;
+        pair_row[p] = row;
+      }
+      if (lane == leader) cnt[wave][sl] += __builtin_popcountll(m);
+      active &= ~m;
+    }
+    __syncthreads();
+  }
+}
+
 __global__ __launch_bounds__(kBlock) void gather_kernel(const uint4* __restrict__ x,
                                                         const int32_t* __restrict__ perm,
                                                         const int32_t* __restrict__ offsets, int S,
@@ -240,6 +357,26 @@ hipError_t remap_dispatch(bool replay, const int32_t* ids, int T, int k, const i
   const size_t hist_bytes = ((size_t)nchunks * S * sizeof(int32_t) + 255) & ~(size_t)255;
   int32_t* hist = static_cast<int32_t*>(ws);
   int32_t* unserved_chunk = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + hist_bytes);
+  if (npairs <= kSmallPairs) {
+    if (replay)
+      hipLaunchKernelGGL(dispatch_one_block_kernel<true>, dim3(1), dim3(kOneBlock), 0, stream, ids,
+                         npairs, k, ert, E, R, alive, S, nullptr, prior, pair_slot, counts,
+                         offsets, perm, pair_row, n_unserved, total_out);
+    else
+      hipLaunchKernelGGL(dispatch_one_block_kernel<false>, dim3(1), dim3(kOneBlock), 0, stream,
+                         ids, npairs, k, ert, E, R, alive, S, token_valid, nullptr, pair_slot,
+                         counts, offsets, perm, pair_row, n_unserved, total_out);
+    if (x_perm && npairs > 0) {
+      const int nch = d / 8;
+      const long maxq = (long)npairs * nch;
+      const long blocks = (maxq + kBlock - 1) / kBlock;
+      const int grid = (int)(blocks < 8192 ? blocks : 8192);
+      hipLaunchKernelGGL(gather_kernel, dim3(grid), dim3(kBlock), 0, stream,
+                         reinterpret_cast<const uint4*>(x), perm, offsets, S, k, nch,
+                         reinterpret_cast<uint4*>(x_perm));
+    }
+    return hipGetLastError();
+  }
   if (nchunks > 0) {
     if (replay)
       hipLaunchKernelGGL(remap_count_kernel<true>, dim3(nchunks), dim3(kBlock), 0, stream, ids,

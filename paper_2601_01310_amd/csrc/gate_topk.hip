@@ -8,8 +8,9 @@
 // tokens) stages it in LDS once, so the matrix is read from memory once per
 // 16 tokens instead of once per token. Top-k runs as k rounds of a wave
 // arg-max over the float32 logits (larger first, ties to the lower expert
-// id); lane j keeps the j-th winner, the k exponentials are formed in
-// parallel and summed in rank order.
+// id), the cross-lane step in DPP row operations and lane reads; lane j
+// keeps the j-th winner, the k exponentials are formed in parallel and
+// summed in rank order.
 #include "tg_device.h"
 #include "tg_launch.h"
 
@@ -17,7 +18,6 @@ namespace tg {
 namespace {
 
 constexpr int kWaves = 4;          // waves per block (unstaged kernels)
-constexpr int kMaxEPerLane = 16;   // E <= 1024
 constexpr int kStagedWaves = 16;   // waves (= tokens) per block when the gate matrix is staged
 constexpr int kStageElems = 48 * 1024;  // 96 KB of bf16
 constexpr int kStagedMaxE = kStageElems / 256;  // staged only when E * d fits, d >= 256
@@ -26,56 +26,92 @@ __device__ __forceinline__ bool better(float v, int id, float bv, int bid) {
   return v > bv || (v == bv && id < bid);
 }
 
-// Top-k over the logits held in `lg` (LDS, E floats) by one wave; writes
-// ids and weights of token t.
+// Arg-max of (v, id) over the 16 lanes of each DPP row: xor 1, xor 2
+// (quad permutes), then half-row and row mirrors; afterwards every lane of a
+// row holds the row's best.
+__device__ __forceinline__ void row_best(float& bv, int& bid) {
+#define TG_DPP_STEP(ctrl)                                                                 \
+  do {                                                                                    \
+    const float ov = __int_as_float(                                                      \
+        __builtin_amdgcn_update_dpp(0, __float_as_int(bv), ctrl, 0xF, 0xF, false));       \
+    const int oid = __builtin_amdgcn_update_dpp(0, bid, ctrl, 0xF, 0xF, false);           \
+    if (better(ov, oid, bv, bid)) {                                                       \
+      bv = ov;                                                                            \
+      bid = oid;                                                                          \
+    }                                                                                     \
+  } while (0)
+  TG_DPP_STEP(0xB1);   // quad_perm [1,0,3,2]
+  TG_DPP_STEP(0x4E);   // quad_perm [2,3,0,1]
+  TG_DPP_STEP(0x141);  // row_half_mirror
+  TG_DPP_STEP(0x140);  // row_mirror
+#undef TG_DPP_STEP
+}
+
+// Top-k over the logits held in `lg` (LDS, E <= 64 * NQ floats) by one
+// wave; writes ids and weights of token t. Each round takes the best
+// remaining candidate of every lane, reduces the rows with DPP and the four
+// rows with lane reads, so no round goes through LDS.
+template <int NQ>
 __device__ void wave_topk(const float* lg, int E, int k, int t, int32_t* __restrict__ ids,
                           float* __restrict__ w) {
   const int lane = lane_id();
-  float v[kMaxEPerLane];
-  uint32_t taken = 0;
-  const int nq = (E + kWave - 1) / kWave;
+  float v[NQ];
 #pragma unroll
-  for (int q = 0; q < kMaxEPerLane; ++q) {
+  for (int q = 0; q < NQ; ++q) {
     const int e = lane + q * kWave;
-    v[q] = (q < nq && e < E) ? lg[e] : 0.0f;
+    v[q] = (e < E) ? lg[e] : 0.0f;
   }
+  uint32_t taken = 0;
   float my_v = 0.0f;
   int my_id = 0;
   for (int j = 0; j < k; ++j) {
     float bv = -__builtin_inff();
     int bid = 0x7fffffff;
 #pragma unroll
-    for (int q = 0; q < kMaxEPerLane; ++q) {
+    for (int q = 0; q < NQ; ++q) {
       const int e = lane + q * kWave;
-      if (q < nq && e < E && !(taken & (1u << q)) && better(v[q], e, bv, bid)) {
+      if (e < E && !(taken & (1u << q)) && better(v[q], e, bv, bid)) {
         bv = v[q];
         bid = e;
       }
     }
+    row_best(bv, bid);
+    float gv = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(bv), 0));
+    int gid = __builtin_amdgcn_readlane(bid, 0);
 #pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) {
-      const float ov = __shfl_xor(bv, off);
-      const int oid = __shfl_xor(bid, off);
-      if (better(ov, oid, bv, bid)) {
-        bv = ov;
-        bid = oid;
+    for (int r = 1; r < 4; ++r) {
+      const float rv = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(bv), 16 * r));
+      const int rid = __builtin_amdgcn_readlane(bid, 16 * r);
+      if (better(rv, rid, gv, gid)) {
+        gv = rv;
+        gid = rid;
       }
     }
-    if ((bid % kWave) == lane) taken |= 1u << (bid / kWave);
+    if ((gid & (kWave - 1)) == lane) taken |= 1u << (gid / kWave);
     if (lane == j) {
-      my_v = bv;
-      my_id = bid;
+      my_v = gv;
+      my_id = gid;
     }
   }
   // w_j = exp(l_j - l_0) / sum_{j'<k} exp(l_j' - l_0), the sum in rank order.
-  const float v0 = __shfl(my_v, 0);
+  const float v0 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(my_v), 0));
   const float ex = (lane < k) ? expf(my_v - v0) : 0.0f;
   float z = 0.0f;
-  for (int j = 0; j < k; ++j) z += __shfl(ex, j);
+  for (int j = 0; j < k; ++j) z += __int_as_float(__builtin_amdgcn_readlane(__float_as_int(ex), j));
   if (lane < k) {
     ids[(size_t)t * k + lane] = my_id;
     w[(size_t)t * k + lane] = ex / z;
   }
+}
+
+// wave_topk for the smallest NQ that covers E.
+__device__ __forceinline__ void wave_topk_any(const float* lg, int E, int k, int t,
+                                              int32_t* __restrict__ ids, float* __restrict__ w) {
+  if (E <= 64) wave_topk<1>(lg, E, k, t, ids, w);
+  else if (E <= 128) wave_topk<2>(lg, E, k, t, ids, w);
+  else if (E <= 256) wave_topk<4>(lg, E, k, t, ids, w);
+  else if (E <= 512) wave_topk<8>(lg, E, k, t, ids, w);
+  else wave_topk<16>(lg, E, k, t, ids, w);
 }
 
 // float64 logits of token t for experts e0..e0+7 against a gate matrix
@@ -157,7 +193,7 @@ __global__ __launch_bounds__(STAGED ? 64 * kStagedWaves : 64 * kWaves) void gate
     if (logits_out) {
       for (int e = lane; e < E; e += kWave) logits_out[(size_t)t * E + e] = lg[e];
     }
-    wave_topk(lg, E, k, t, ids, w);
+    wave_topk_any(lg, E, k, t, ids, w);
   }
 }
 
@@ -173,7 +209,7 @@ __global__ __launch_bounds__(256) void logits_topk_kernel(const float* __restric
   for (int e = lane; e < E; e += kWave) lg[e] = logits[(size_t)t * E + e];
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  wave_topk(lg, E, k, t, ids, w);
+  wave_topk_any(lg, E, k, t, ids, w);
 }
 
 }  // namespace
