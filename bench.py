@@ -61,6 +61,10 @@ class HipEvents:
             out.append(ev.value)
         return out
 
+    def record(self, ev, stream):
+        if self.hip.hipEventRecord(ctypes.c_void_p(ev), ctypes.c_void_p(stream.cuda_stream)) != 0:
+            raise RuntimeError("hipEventRecord failed")
+
     def elapsed_ms(self, a, b):
         ms = ctypes.c_float()
         if self.hip.hipEventElapsedTime(ctypes.byref(ms), ctypes.c_void_p(a), ctypes.c_void_p(b)) != 0:
@@ -391,25 +395,38 @@ def main():
     stream = torch.cuda.current_stream()
 
     def timed_steps(n):
-        """n steps of the whole path; per-stage and per-step event times (ms)
-        and the host wall time per step."""
-        evs = hip.create(6 * n)
+        """n plain steps of the whole path: host wall time per step and the
+        sorted per-step times from one pair of events around each step."""
+        evs = hip.create(n + 1)
         torch.cuda.synchronize()
         t0 = time.perf_counter()
+        hip.record(evs[0], stream)
+        for i in range(n):
+            tg.tg_ew_forward(f.args, f.ws, f.ws_bytes, stream)
+            hip.record(evs[i + 1], stream)
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        per = sorted(hip.elapsed_ms(evs[i], evs[i + 1]) for i in range(n))
+        hip.destroy(evs)
+        return per, (t1 - t0) * 1e3 / n
+
+    def stage_times(n):
+        """Mean per-stage times over n steps with events between the stages
+        (a separate pass: the events add a little time between kernels)."""
+        evs = hip.create(6 * n)
+        torch.cuda.synchronize()
         for i in range(n):
             tg.tg_ew_forward_timed(f.args, f.ws, f.ws_bytes, evs[6 * i:6 * i + 6], stream)
         torch.cuda.synchronize()
-        t1 = time.perf_counter()
-        stages = [[hip.elapsed_ms(evs[6 * i + j], evs[6 * i + j + 1]) for j in range(5)]
-                  for i in range(n)]
+        st = [sum(hip.elapsed_ms(evs[6 * i + j], evs[6 * i + j + 1]) for i in range(n)) / n
+              for j in range(5)]
         hip.destroy(evs)
-        return stages, (t1 - t0) * 1e3 / n
+        return st
 
     for _ in range(args.warmup):
         f(stream)
-    per_step, ms = timed_steps(args.steps)
-    stage_ms = [sum(st[j] for st in per_step) / args.steps for j in range(5)]
-    step_ev = sorted(sum(st) for st in per_step)
+    step_ev, ms = timed_steps(args.steps)
+    stage_ms = stage_times(args.steps)
     P = int(f.slot_offsets[-1])
     counts = f.slot_counts.cpu()
     touched = int((counts > 0).sum())
@@ -421,8 +438,7 @@ def main():
         f.set_alive(wl.alive_after_failure())
         for _ in range(args.warmup):
             f(stream)
-        fo_steps, fo_ms = timed_steps(args.steps)
-        fo_ev = sorted(sum(st) for st in fo_steps)
+        fo_ev, fo_ms = timed_steps(args.steps)
         failover = {"ms_per_step": fo_ms, "step_ms_p50": fo_ev[len(fo_ev) // 2],
                     "routed_pairs": int(f.slot_offsets[-1])}
         f.set_alive(wl.alive)

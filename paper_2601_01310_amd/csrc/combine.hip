@@ -2,22 +2,22 @@
 // in float32, in rank order j = 0..k-1, skipping pairs not routed here; and
 // the merge step of a replay (§5.1), which re-forms the same sum for the
 // tokens whose pairs were recomputed on another slot.
-// One block per token; each thread owns 8-element (16-byte) column chunks,
-// so the y rows are read and the output row written fully coalesced.
+// One block per token; threads own 8-element (16-byte) column chunks, so a
+// token's k rows are read and its output row written fully coalesced.
 #include "tg_device.h"
 #include "tg_launch.h"
 
 namespace tg {
 namespace {
 
-constexpr int kBlock = 256;
+constexpr int kMaxBlock = 1024;
 
 // rows[j] >= 0: y row; rows[j] <= -2: row -rows[j]-2 of y2; -1: no output.
 __device__ __forceinline__ void combine_row(const uint4* __restrict__ y,
                                             const uint4* __restrict__ y2, const int* rows,
                                             const float* ws, int t, int k, int nch,
                                             uint4* __restrict__ out) {
-  for (int c = threadIdx.x; c < nch; c += kBlock) {
+  for (int c = threadIdx.x; c < nch; c += blockDim.x) {
     float acc[8];
 #pragma unroll
     for (int i = 0; i < 8; ++i) acc[i] = 0.0f;
@@ -42,7 +42,7 @@ __device__ __forceinline__ void combine_row(const uint4* __restrict__ y,
   }
 }
 
-__global__ __launch_bounds__(kBlock) void combine_kernel(const uint4* __restrict__ y,
+__global__ __launch_bounds__(kMaxBlock) void combine_kernel(const uint4* __restrict__ y,
                                                          const int32_t* __restrict__ pair_row,
                                                          const float* __restrict__ w, int T, int k,
                                                          int nch, uint4* __restrict__ out) {
@@ -60,7 +60,7 @@ __global__ __launch_bounds__(kBlock) void combine_kernel(const uint4* __restrict
 
 // One block per token; tokens whose pairs all keep their first-pass result
 // return at once.
-__global__ __launch_bounds__(kBlock) void recombine_kernel(
+__global__ __launch_bounds__(kMaxBlock) void recombine_kernel(
     const uint4* __restrict__ y, const int32_t* __restrict__ pair_row,
     const int32_t* __restrict__ prior, const uint8_t* __restrict__ alive, int S,
     const uint4* __restrict__ y2, const int32_t* __restrict__ replay_row,
@@ -93,10 +93,21 @@ __global__ __launch_bounds__(kBlock) void recombine_kernel(
 
 }  // namespace
 
+// Threads per block. Few tokens (a decode step): one thread per 16-byte
+// chunk of a row, in whole waves, so each block issues all its loads at
+// once. Many tokens: 256 threads looping over the chunks, which keeps more
+// blocks resident per CU.
+static int combine_block(int T, int d) {
+  if (T > 2048) return 256;
+  const int nch = d / 8;
+  const int b = (nch + kWave - 1) / kWave * kWave;
+  return b < kMaxBlock ? b : kMaxBlock;
+}
+
 hipError_t launch_combine(const uint16_t* y, const int32_t* pair_row, const float* w, int T, int k,
                           int d, uint16_t* out, hipStream_t stream) {
   if (T == 0) return hipSuccess;
-  hipLaunchKernelGGL(combine_kernel, dim3(T), dim3(kBlock), 0, stream,
+  hipLaunchKernelGGL(combine_kernel, dim3(T), dim3(combine_block(T, d)), 0, stream,
                      reinterpret_cast<const uint4*>(y), pair_row, w, T, k, d / 8,
                      reinterpret_cast<uint4*>(out));
   return hipGetLastError();
@@ -107,7 +118,7 @@ hipError_t launch_recombine(const uint16_t* y, const int32_t* pair_row, const in
                             const int32_t* replay_row, const float* w, int T, int k, int d,
                             uint16_t* out, hipStream_t stream) {
   if (T == 0) return hipSuccess;
-  hipLaunchKernelGGL(recombine_kernel, dim3(T), dim3(kBlock), 0, stream,
+  hipLaunchKernelGGL(recombine_kernel, dim3(T), dim3(combine_block(T, d)), 0, stream,
                      reinterpret_cast<const uint4*>(y), pair_row, prior_slot, alive, S,
                      reinterpret_cast<const uint4*>(y2), replay_row, w, T, k, d / 8,
                      reinterpret_cast<uint4*>(out));
