@@ -334,6 +334,100 @@ def partial_batch_cost(wl, steps, warmup, n_aws=8, late=(3,)):
     return res
 
 
+def checkpoint_cost(wl, steps, warmup):
+    """KV-segment checkpoint of one decode step (§6.1; Mixtral segments of
+    2 * 8 KV heads * 128 * 2 bytes, App. C) for 128 requests over 32 layers
+    into pinned host memory: its time alone, and the EW forward's time alone
+    and with the checkpoint running on a second stream."""
+    import numpy as np
+    import torch
+    from ctypes import c_void_p
+
+    from paper_2601_01310_amd import tg
+
+    dev = wl.x.device
+    hip = HipEvents()
+    main_s = torch.cuda.current_stream()
+    side = torch.cuda.Stream()
+    seg, layers, requests, max_len = 4096, 32, 128, 64
+    size = layers * requests * max_len * seg
+    kv = torch.empty(size, dtype=torch.uint8, device=dev)
+    kv.random_(0, 256)
+    store = torch.empty(size, dtype=torch.uint8, pin_memory=True)
+    log_cap = layers * requests
+    log = torch.zeros(log_cap * 3, dtype=torch.int64, pin_memory=True)
+    commit = torch.zeros(1, dtype=torch.int64, pin_memory=True)
+    pos = 7
+    offs = np.array([((l * requests + r) * max_len + pos) * seg for r in range(requests)
+                     for l in range(layers)], dtype=np.int64)
+    n = len(offs)
+    od = torch.from_numpy(offs).to(dev)
+    bd = torch.full((n,), seg, dtype=torch.int32, device=dev)
+    f = tg.EwForward(wl)
+    seq = [0]
+
+    blocks = [0]
+
+    def ckpt(stream):
+        tg.tg_kv_checkpoint(kv, size, od, bd, n, seq[0], store, log, log_cap, commit, stream,
+                            max_blocks=blocks[0])
+        seq[0] += n
+
+    def timed(fn, stream):
+        for _ in range(warmup):
+            fn()
+        ev = hip.create(2 * steps)
+        torch.cuda.synchronize()
+        for i in range(steps):
+            hip.hip.hipEventRecord(c_void_p(ev[2 * i]), c_void_p(stream.cuda_stream))
+            fn()
+            hip.hip.hipEventRecord(c_void_p(ev[2 * i + 1]), c_void_p(stream.cuda_stream))
+        torch.cuda.synchronize()
+        us = sorted(hip.elapsed_ms(ev[2 * i], ev[2 * i + 1]) * 1e3 for i in range(steps))
+        hip.destroy(ev)
+        return us[len(us) // 2]
+
+    def both():
+        side.wait_stream(main_s)
+        ckpt(side)
+        f(main_s)
+        main_s.wait_stream(side)
+
+    fwd_us = timed(lambda: f(main_s), main_s)
+    paths = {}
+    for g in (8, 16, 32):
+        blocks[0] = g
+        ck_us = timed(lambda: ckpt(main_s), main_s)
+        both_us = timed(both, main_s)
+        paths[f"kernel_{g}_blocks"] = {
+            "checkpoint_us_p50": ck_us, "checkpoint_gbps": n * seg / ck_us / 1e3,
+            "forward_with_concurrent_checkpoint_us_p50": both_us}
+    # The same batch is strided (pitch = max_len segments): copy engine.
+    first, pitch = pos * seg, max_len * seg
+
+    def strided(stream):
+        tg.tg_kv_checkpoint_strided(kv, size, first, pitch, seg, n, seq[0], store, log, log_cap,
+                                    commit, stream)
+        seq[0] += n
+
+    def both_strided():
+        side.wait_stream(main_s)
+        strided(side)
+        f(main_s)
+        main_s.wait_stream(side)
+
+    ck_us = timed(lambda: strided(main_s), main_s)
+    paths["copy_engine_strided"] = {
+        "checkpoint_us_p50": ck_us, "checkpoint_gbps": n * seg / ck_us / 1e3,
+        "forward_with_concurrent_checkpoint_us_p50": timed(both_strided, main_s)}
+    torch.cuda.synchronize()
+    res = {"workload": wl.name, "segments": n, "segment_bytes": seg,
+           "checkpoint_bytes": n * seg, "forward_us_p50": fwd_us, "paths": paths,
+           "commit": int(commit[0])}
+    print(json.dumps(res), flush=True)
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -348,6 +442,9 @@ def main():
                          "point instead of the benchmark line)")
     ap.add_argument("--shadow", action="store_true",
                     help="idle-shadow / concurrent-expert interference check (one JSON line)")
+    ap.add_argument("--ckpt", action="store_true",
+                    help="KV-segment checkpoint of one decode step: alone and alongside the "
+                         "forward (one JSON line)")
     ap.add_argument("--partial", action="store_true",
                     help="partial-batch trigger + forward against the full forward (one JSON line)")
     ap.add_argument("--replay", action="store_true",
@@ -388,6 +485,9 @@ def main():
         return
     if args.partial:
         partial_batch_cost(wl, args.steps, args.warmup)
+        return
+    if args.ckpt:
+        checkpoint_cost(wl, args.steps, args.warmup)
         return
     alive = wl.alive_after_failure() if args.failover else wl.alive
     f = tg.EwForward(wl, alive)

@@ -252,6 +252,65 @@ tg_status tg_batch_trigger(const uint32_t* delivered, const uint8_t* aw_alive,
                            long long spin_limit, uint8_t* token_valid, int32_t* status,
                            void* stream);
 
+/*
+ * Incremental KV-segment checkpoint (§6.1) and request-level restoration
+ * (§6.2), on one GPU: host-visible memory (pinned host memory, or any
+ * memory the GPU can write) plays the checkpoint store.
+ *
+ * The store has the KV region's layout: a segment at byte offset o of the
+ * KV region is stored at byte offset o of the store (both buffers
+ * kv_bytes long and 16-byte aligned). tg_kv_checkpoint copies n segments
+ * (seg_offset [n] uint64 byte offsets, seg_bytes [n] uint32 lengths, device
+ * arrays; both multiples of 16 and inside the region) from the device KV
+ * region to the store, tags segment i with sequence number first_seq + i,
+ * writes its record {seq, offset, bytes} to log[seq % log_cap] (bytes 0 when
+ * the segment was rejected as misaligned or out of range; the log is a ring,
+ * so it keeps the last log_cap records), and, once every
+ * copy and record has landed, stores first_seq + n into *commit (the
+ * "log + commit record" of §6.1: every sequence number below the commit
+ * record has landed; 0 = nothing committed; commit may be NULL to leave the
+ * batch uncommitted). Calls on one stream commit in order; the caller gives
+ * consecutive, increasing sequence numbers across calls. The copy runs on
+ * at most max_blocks workgroups (0 = 16), so that it can proceed on a
+ * second stream beside the caller's compute (the gaps of §6.1) while taking
+ * few CUs from it.
+ *
+ * tg_kv_restore copies n committed segments from the store back into a
+ * device KV region (src [n] store offsets, dst [n] offsets in kv_dst, bytes
+ * [n], seq [n] their sequence numbers): a segment whose seq is not below
+ * the commit record read at the start of the kernel is skipped. status [n]
+ * uint8: 1 restored, 0 not committed, 2 misaligned or out of range.
+ */
+typedef struct {
+  uint64_t seq;
+  uint64_t offset;
+  uint64_t bytes;
+} tg_ckpt_record;
+
+tg_status tg_kv_checkpoint(const void* kv, size_t kv_bytes, const uint64_t* seg_offset,
+                           const uint32_t* seg_bytes, int n, uint64_t first_seq, void* store,
+                           tg_ckpt_record* log, int log_cap, uint64_t* commit, int max_blocks,
+                           void* stream);
+/*
+ * tg_kv_checkpoint for n segments at a constant stride: segment i is at
+ * byte offset first_offset + i * pitch and is seg_bytes long (one decode
+ * step of a [layer][request][position][segment] region is such a batch).
+ * The bytes move by one strided copy on the GPU's copy engine, so no
+ * compute unit is taken from concurrent work; the records and the commit
+ * record follow in one small kernel, after the copy in stream order.
+ * Offsets, pitch and seg_bytes must be multiples of 16 with seg_bytes <=
+ * pitch, and the batch must lie inside the region (checked on the host:
+ * TG_ERR_BAD_DIM otherwise).
+ */
+tg_status tg_kv_checkpoint_strided(const void* kv, size_t kv_bytes, uint64_t first_offset,
+                                   uint64_t pitch, uint32_t seg_bytes, int n, uint64_t first_seq,
+                                   void* store, tg_ckpt_record* log, int log_cap,
+                                   uint64_t* commit, void* stream);
+tg_status tg_kv_restore(const void* store, size_t store_bytes, const uint64_t* commit,
+                        const uint64_t* seq, const uint64_t* src, const uint64_t* dst,
+                        const uint32_t* bytes, int n, void* kv_dst, size_t kv_bytes,
+                        uint8_t* status, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

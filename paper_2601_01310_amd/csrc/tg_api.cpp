@@ -407,4 +407,68 @@ tg_status tg_batch_trigger(const uint32_t* delivered, const uint8_t* aw_alive,
                     "tg_batch_trigger");
 }
 
+// Blocks a checkpoint copy occupies by default: enough to keep the host
+// link busy while leaving nearly every CU to concurrent compute.
+constexpr int kCkptBlocks = 16;
+
+static bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+
+tg_status tg_kv_checkpoint(const void* kv, size_t kv_bytes, const uint64_t* seg_offset,
+                           const uint32_t* seg_bytes, int n, uint64_t first_seq, void* store,
+                           tg_ckpt_record* log, int log_cap, uint64_t* commit, int max_blocks,
+                           void* stream) {
+  if (n < 0) return fail(TG_ERR_BAD_DIM, "n=%d must be >= 0", n);
+  if (max_blocks < 0) return fail(TG_ERR_BAD_DIM, "max_blocks=%d must be >= 0", max_blocks);
+  if (n > 0 && log_cap <= 0) return fail(TG_ERR_BAD_DIM, "log_cap=%d must be > 0", log_cap);
+  if (!kv || !store || (n > 0 && (!seg_offset || !seg_bytes || !log)))
+    return fail(TG_ERR_NULL_ARG, "a required pointer is NULL");
+  if (!aligned16(kv) || !aligned16(store) || !aligned16(log))
+    return fail(TG_ERR_UNSUPPORTED, "kv, store and log must be 16-byte aligned");
+  return hip_status(tg::launch_kv_checkpoint(kv, kv_bytes, seg_offset, seg_bytes, n, first_seq,
+                                             store, log, log_cap, commit,
+                                             max_blocks ? max_blocks : kCkptBlocks,
+                                             static_cast<hipStream_t>(stream)),
+                    "tg_kv_checkpoint");
+}
+
+tg_status tg_kv_checkpoint_strided(const void* kv, size_t kv_bytes, uint64_t first_offset,
+                                   uint64_t pitch, uint32_t seg_bytes, int n, uint64_t first_seq,
+                                   void* store, tg_ckpt_record* log, int log_cap,
+                                   uint64_t* commit, void* stream) {
+  if (n < 0) return fail(TG_ERR_BAD_DIM, "n=%d must be >= 0", n);
+  if (n > 0 && log_cap <= 0) return fail(TG_ERR_BAD_DIM, "log_cap=%d must be > 0", log_cap);
+  if (!kv || !store || (n > 0 && !log)) return fail(TG_ERR_NULL_ARG, "a required pointer is NULL");
+  if (!aligned16(kv) || !aligned16(store) || !aligned16(log))
+    return fail(TG_ERR_UNSUPPORTED, "kv, store and log must be 16-byte aligned");
+  if (n > 0) {
+    if (first_offset % 16 || pitch % 16 || seg_bytes % 16 || seg_bytes == 0 || pitch < seg_bytes)
+      return fail(TG_ERR_BAD_DIM, "offsets, pitch and segment size must be multiples of 16, "
+                  "with seg_bytes <= pitch");
+    const unsigned __int128 end =
+        (unsigned __int128)first_offset + (unsigned __int128)(n - 1) * pitch + seg_bytes;
+    if (end > kv_bytes)
+      return fail(TG_ERR_BAD_DIM, "the last segment ends past the region (%zu bytes)", kv_bytes);
+  }
+  return hip_status(tg::launch_kv_checkpoint_strided(kv, first_offset, pitch, seg_bytes, n,
+                                                     first_seq, store, log, log_cap, commit,
+                                                     static_cast<hipStream_t>(stream)),
+                    "tg_kv_checkpoint_strided");
+}
+
+tg_status tg_kv_restore(const void* store, size_t store_bytes, const uint64_t* commit,
+                        const uint64_t* seq, const uint64_t* src, const uint64_t* dst,
+                        const uint32_t* bytes, int n, void* kv_dst, size_t kv_bytes,
+                        uint8_t* status, void* stream) {
+  if (n < 0) return fail(TG_ERR_BAD_DIM, "n=%d must be >= 0", n);
+  if (!store || !commit || !kv_dst ||
+      (n > 0 && (!seq || !src || !dst || !bytes || !status)))
+    return fail(TG_ERR_NULL_ARG, "a required pointer is NULL");
+  if (!aligned16(store) || !aligned16(kv_dst))
+    return fail(TG_ERR_UNSUPPORTED, "store and kv_dst must be 16-byte aligned");
+  return hip_status(tg::launch_kv_restore(store, store_bytes, commit, seq, src, dst, bytes, n,
+                                          kv_dst, kv_bytes, status,
+                                          static_cast<hipStream_t>(stream)),
+                    "tg_kv_restore");
+}
+
 }  // extern "C"

@@ -6,6 +6,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include "tg.h"
+
 namespace tg {
 
 hipError_t launch_gate_topk(const uint16_t* x, const uint16_t* wg, const float* logits_in, int T,
@@ -72,5 +74,22 @@ hipError_t launch_batch_trigger(const uint32_t* delivered, const uint8_t* aw_ali
                                 const int32_t* chunk_rows, int A, int T, int min_rows,
                                 long long spin_limit, uint8_t* token_valid, int32_t* status,
                                 hipStream_t stream);
+
+// KV-segment checkpoint / restoration (one block per segment; the commit
+// record is written by a second kernel after the copies).
+hipError_t launch_kv_checkpoint(const void* kv, size_t kv_bytes, const uint64_t* seg_off,
+                                const uint32_t* seg_bytes, int n, uint64_t first_seq, void* store,
+                                tg_ckpt_record* log, int log_cap, uint64_t* commit, int max_blocks,
+                                hipStream_t stream);
+// Strided batch: segment i at first_offset + i * pitch (validated by the
+// caller); copy engine for the bytes, one kernel for the records and commit.
+hipError_t launch_kv_checkpoint_strided(const void* kv, uint64_t first_offset, uint64_t pitch,
+                                        uint32_t seg_bytes, int n, uint64_t first_seq,
+                                        void* store, tg_ckpt_record* log, int log_cap,
+                                        uint64_t* commit, hipStream_t stream);
+hipError_t launch_kv_restore(const void* store, size_t store_bytes, const uint64_t* commit,
+                             const uint64_t* seq, const uint64_t* src, const uint64_t* dst,
+                             const uint32_t* bytes, int n, void* kv, size_t kv_bytes,
+                             uint8_t* status, hipStream_t stream);
 
 }  // namespace tg

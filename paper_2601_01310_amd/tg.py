@@ -22,7 +22,7 @@ EXPORTS = [
     "tg_status_string", "tg_last_error", "tg_gate_topk", "tg_remap_dispatch_workspace",
     "tg_remap_dispatch", "tg_expert_ffn_grouped", "tg_combine", "tg_ew_forward_workspace",
     "tg_ew_forward", "tg_ew_forward_timed", "tg_ew_replay_workspace", "tg_ew_replay",
-    "tg_batch_trigger",
+    "tg_batch_trigger", "tg_kv_checkpoint", "tg_kv_checkpoint_strided", "tg_kv_restore",
 ]
 
 
@@ -92,6 +92,14 @@ def load(path: Optional[str] = None):
     lib.tg_ew_replay.argtypes = [ctypes.POINTER(ReplayArgs), vp, sz, vp]
     lib.tg_batch_trigger.restype = i
     lib.tg_batch_trigger.argtypes = [vp, vp, vp, i, i, i, ctypes.c_longlong, vp, vp, vp]
+    u64 = ctypes.c_uint64
+    lib.tg_kv_checkpoint.restype = i
+    lib.tg_kv_checkpoint.argtypes = [vp, sz, vp, vp, i, u64, vp, vp, i, vp, i, vp]
+    lib.tg_kv_checkpoint_strided.restype = i
+    lib.tg_kv_checkpoint_strided.argtypes = [vp, sz, u64, u64, ctypes.c_uint32, i, u64, vp, vp, i,
+                                             vp, vp]
+    lib.tg_kv_restore.restype = i
+    lib.tg_kv_restore.argtypes = [vp, sz, vp, vp, vp, vp, vp, i, vp, sz, vp, vp]
     _lib = lib
     return lib
 
@@ -202,10 +210,37 @@ def tg_batch_trigger(delivered, aw_alive, chunk_rows, A, T, min_rows, spin_limit
                                    _stream(stream)), "tg_batch_trigger")
 
 
+def tg_kv_checkpoint(kv, kv_bytes, seg_offset, seg_bytes, n, first_seq, store, log, log_cap,
+                     commit, stream=None, max_blocks=0):
+    """``store``, ``log`` ([log_cap, 3] uint64) and ``commit`` ([1] uint64)
+    may be pinned host tensors or device tensors; ``commit`` may be None."""
+    _check(load().tg_kv_checkpoint(_p(kv), kv_bytes, _p(seg_offset), _p(seg_bytes), n, first_seq,
+                                   _flag_ptr(store), _flag_ptr(log), log_cap,
+                                   None if commit is None else _flag_ptr(commit), max_blocks,
+                                   _stream(stream)), "tg_kv_checkpoint")
+
+
+def tg_kv_checkpoint_strided(kv, kv_bytes, first_offset, pitch, seg_bytes, n, first_seq, store,
+                             log, log_cap, commit, stream=None):
+    _check(load().tg_kv_checkpoint_strided(_p(kv), kv_bytes, first_offset, pitch, seg_bytes, n,
+                                           first_seq, _flag_ptr(store), _flag_ptr(log), log_cap,
+                                           None if commit is None else _flag_ptr(commit),
+                                           _stream(stream)), "tg_kv_checkpoint_strided")
+
+
+def tg_kv_restore(store, store_bytes, commit, seq, src, dst, nbytes, n, kv_dst, kv_bytes, status,
+                  stream=None):
+    _check(load().tg_kv_restore(_flag_ptr(store), store_bytes, _flag_ptr(commit), _p(seq), _p(src),
+                                _p(dst), _p(nbytes), n, _p(kv_dst), kv_bytes, _p(status),
+                                _stream(stream)), "tg_kv_restore")
+
+
 def _flag_ptr(t):
+    """Device tensors as usual; a pinned host tensor is passed by its address,
+    which the GPU can use directly."""
     if isinstance(t, torch.Tensor) and t.device.type == "cpu":
         if not t.is_pinned() or not t.is_contiguous():
-            raise ValueError("host flags must be a contiguous pinned tensor")
+            raise ValueError("host buffers must be contiguous pinned tensors")
         return t.data_ptr()  # pinned host memory is mapped at the same address on the device
     return _p(t)
 

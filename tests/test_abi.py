@@ -188,6 +188,25 @@ def test_batch_trigger_rejects_bad_arguments(lib):
     assert call(st=None) == tg.TG_ERR_NULL_ARG
 
 
+def test_kv_checkpoint_entry_points_reject_bad_arguments(lib):
+    A = 0x10000  # 16-byte aligned bogus addresses
+    assert lib.tg_kv_checkpoint(A, 1 << 20, A, A, -1, 0, A, A, 8, None, 0, None) == tg.TG_ERR_BAD_DIM
+    assert lib.tg_kv_checkpoint(A, 1 << 20, A, A, 4, 0, A, A, 0, None, 0, None) == tg.TG_ERR_BAD_DIM
+    assert lib.tg_kv_checkpoint(A, 1 << 20, A, A, 4, 0, A, A, 8, None, -1, None) == tg.TG_ERR_BAD_DIM
+    assert lib.tg_kv_checkpoint(A, 1 << 20, None, A, 4, 0, A, A, 8, None, 0, None) == tg.TG_ERR_NULL_ARG
+    assert lib.tg_kv_checkpoint(A + 8, 1 << 20, A, A, 4, 0, A, A, 8, None, 0, None) == \
+        tg.TG_ERR_UNSUPPORTED
+    s = lib.tg_kv_checkpoint_strided
+    assert s(A, 1 << 20, 0, 4096, 4096, 257, 0, A, A, 8, None, None) == tg.TG_ERR_BAD_DIM  # past end
+    assert s(A, 1 << 20, 8, 4096, 4096, 4, 0, A, A, 8, None, None) == tg.TG_ERR_BAD_DIM   # misaligned
+    assert s(A, 1 << 20, 0, 2048, 4096, 4, 0, A, A, 8, None, None) == tg.TG_ERR_BAD_DIM   # overlap
+    assert s(A, 1 << 20, 0, 4096, 4096, 4, 0, A, None, 8, None, None) == tg.TG_ERR_NULL_ARG
+    r = lib.tg_kv_restore
+    assert r(A, 1 << 20, None, A, A, A, A, 4, A, 1 << 20, A, None) == tg.TG_ERR_NULL_ARG
+    assert r(A, 1 << 20, A, A, A, A, A, -1, A, 1 << 20, A, None) == tg.TG_ERR_BAD_DIM
+    assert r(A, 1 << 20, A, A, A, A, A, 4, A + 4, 1 << 20, A, None) == tg.TG_ERR_UNSUPPORTED
+
+
 def test_binding_refuses_host_tensors(lib):
     import torch
     with pytest.raises(ValueError):

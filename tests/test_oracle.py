@@ -14,6 +14,7 @@ import pytest
 import scipy.special
 import torch
 
+from oracle import kv_checkpoint as K
 from oracle import moe_ew as O
 from paper_2601_01310_amd import synth
 from tests._util import bf16_bits_to_f32, host, u16, ulp_diff_bf16
@@ -522,3 +523,68 @@ def test_skewed_workload_sends_about_forty_percent_to_the_four_hottest():
     local = ids[ids < 32]
     share = np.isin(local, wl.hot_experts).mean()
     assert 0.38 <= share <= 0.42, share
+
+
+# ---------------------------------------------------------------- KV checkpoint (§6.1, §6.2)
+
+
+def _kv_case(seed=0, size=1 << 16):
+    rng = np.random.default_rng(seed)
+    kv = rng.integers(0, 256, size=size, dtype=np.uint8)
+    return rng, kv
+
+
+def test_segment_sizes_of_app_c_for_mixtral():
+    """Mixtral-8x7B: 8 KV heads of 128 of a 4096 hidden size over 32 heads,
+    bf16: a KV segment is 4 KiB, 12.5 % of the 32 KiB of expert traffic."""
+    C = K.segment_bytes(8, 4096, 32, 2)
+    V = K.expert_traffic_bytes(2, 4096, 2)
+    assert C == 4096 and V == 32768 and C / V == 0.125
+
+
+def test_checkpoint_then_restore_round_trips_committed_segments():
+    rng, kv = _kv_case()
+    store = np.full(kv.size, 0xEE, dtype=np.uint8)
+    log = np.zeros((8, 3), dtype=np.uint64)
+    offs = np.array([0, 4096, 512, 60000], dtype=np.uint64)
+    nbs = np.array([256, 1024, 16, 5536], dtype=np.uint32)
+    store, log, commit = K.checkpoint(kv, store, log, 8, 0, offs, nbs, first_seq=100)
+    assert commit == 104
+    for o, n in zip(offs.tolist(), nbs.tolist()):
+        assert np.array_equal(store[o:o + n], kv[o:o + n])
+    touched = np.zeros(kv.size, bool)
+    for o, n in zip(offs.tolist(), nbs.tolist()):
+        touched[o:o + n] = True
+    assert (store[~touched] == 0xEE).all()
+    assert log[100 % 8].tolist() == [100, 0, 256] and log[103 % 8].tolist() == [103, 60000, 5536]
+    dst = np.zeros(1 << 15, dtype=np.uint8)
+    dsts = np.array([0, 256, 1280, 1296], dtype=np.uint64)
+    out, st = K.restore(store, commit, np.arange(100, 104), offs, dsts, nbs, dst)
+    assert st.tolist() == [1, 1, 1, 1]
+    for o, d, n in zip(offs.tolist(), dsts.tolist(), nbs.tolist()):
+        assert np.array_equal(out[d:d + n], kv[o:o + n])
+
+
+def test_uncommitted_segments_are_not_restored():
+    """A batch whose commit record never landed (the worker died first) is
+    skipped by restoration even though its bytes are in the store."""
+    rng, kv = _kv_case(1)
+    store = np.zeros(kv.size, dtype=np.uint8)
+    log = np.zeros((4, 3), dtype=np.uint64)
+    store, log, c1 = K.checkpoint(kv, store, log, 4, 0, [0], [64], first_seq=0)
+    kv2 = kv.copy()
+    kv2[64:128] ^= 0xFF
+    store, log, c2 = K.checkpoint(kv2, store, log, 4, c1, [64], [64], first_seq=1,
+                                  write_commit=False)
+    assert c2 == c1 == 1
+    out, st = K.restore(store, c2, [0, 1], [0, 64], [0, 64], [64, 64], np.zeros(256, np.uint8))
+    assert st.tolist() == [1, 0] and np.array_equal(out[:64], kv[:64]) and not out[64:].any()
+
+
+def test_misaligned_or_out_of_range_segments_are_rejected():
+    _, kv = _kv_case(2, size=1024)
+    store, log, commit = K.checkpoint(kv, np.zeros(1024, np.uint8), np.zeros((4, 3), np.uint64),
+                                      4, 0, [8, 1008, 0], [16, 32, 48], first_seq=0)
+    assert log[:3, 2].tolist() == [0, 0, 48] and not store[48:].any()
+    _, st = K.restore(store, commit, [2, 2], [0, 0], [0, 1000], [48, 48], np.zeros(1024, np.uint8))
+    assert st.tolist() == [1, 2]
