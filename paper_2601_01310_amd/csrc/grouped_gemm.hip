@@ -431,6 +431,289 @@ __device__ __forceinline__ void gemm_tile(uint16_t* smem, const TileInfo& tile,
   }
 }
 
+// Persistent variant for the gate/up projection with full-size tiles: one
+// block per CU, each walking the tiles of its XCD's contiguous range with a
+// stride of the XCD's block count. The DMA pipeline runs on across tiles:
+// the last stages of one tile issue the first stages of the next, whose
+// slot, rows and (when GATHER) gathered row offsets are found ahead of time
+// with scalar loads, which do not disturb the vector-memory counts that the
+// pipeline waits on. Results go straight from the accumulators to memory
+// (8-byte stores), so the epilogue needs no LDS and overlaps the next
+// tile's first loads. Same MFMA sequence per output element as
+// grouped_gemm_kernel, hence the same bits.
+template <int BM, int BN, int BK, int WM, int WN, bool SWIGLU, bool GATHER>
+__global__ __launch_bounds__(64 * WM * WN) void grouped_gemm_persistent_kernel(
+    const uint16_t* __restrict__ A, const int32_t* __restrict__ offsets, int S,
+    const uint16_t* __restrict__ B, int K, int NW, int I, uint16_t* __restrict__ C, int ldc,
+    int NT, const int32_t* __restrict__ perm, uint32_t kq_magic, int kq_shift, int A_rows) {
+  constexpr int NWAVE = WM * WN;
+  constexpr int MB = BM / WM / 32;
+  constexpr int NB = BN / WN / 32;
+  constexpr int CH = BK / 8;
+  constexpr int RPI = 64 / CH;
+  constexpr int RW = BM / NWAVE;            // staged A rows per wave
+  constexpr int AI = RW / RPI;
+  constexpr int BI = BN / NWAVE / RPI;
+  constexpr int A_ST = BM * BK, B_ST = BN * BK;
+  constexpr int WOUT = SWIGLU ? BN / 2 / WN : BN / WN;
+  static_assert(MB >= 1 && NB >= 1 && AI >= 1 && BI >= 1 && (BK == 32 || BK == 64), "tile");
+  static_assert(!SWIGLU || NB % 2 == 0, "gate/up halves");
+  __shared__ __attribute__((aligned(16))) uint16_t smem[2 * A_ST + 3 * B_ST];
+
+  const int total = count_tiles(offsets, S, BM, NT);
+  const int per_xcd_blocks = gridDim.x / kXcds;
+  const int x = blockIdx.x % kXcds, c = blockIdx.x / kXcds;
+  const int per = (total + kXcds - 1) / kXcds;
+  const int lo = x * per, hi = min(lo + per, total);
+  int L = lo + c;
+  if (L >= hi) return;
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave / WN, wn = wave % WN;
+
+  // Scalar cursor over the slots and over (panel, row block) within the
+  // slot; a block's tiles come in increasing order, at most one stride
+  // apart, so the cursor only moves forward, and no step divides (a
+  // division would borrow vector registers that in-flight loads still
+  // address).
+  int s_cur = 0, before = 0, pos = 0, c_nt = 0, c_m = 0;
+  int o_cur = offsets[0];
+  int cnt_cur = offsets[1] - o_cur;
+  int mt_cur = (cnt_cur + BM - 1) / BM;
+  auto seek = [&](int Lq, int& slot, int& row0, int& rows, int& nt) {
+    while (Lq >= before + mt_cur * NT) {
+      before += mt_cur * NT;
+      ++s_cur;
+      o_cur = offsets[s_cur];
+      cnt_cur = offsets[s_cur + 1] - o_cur;
+      mt_cur = (cnt_cur + BM - 1) / BM;
+      pos = before;
+      c_nt = 0;
+      c_m = 0;
+    }
+    for (c_m += Lq - pos; c_m >= mt_cur; c_m -= mt_cur) ++c_nt;
+    pos = Lq;
+    slot = s_cur;
+    nt = c_nt;
+    row0 = o_cur + c_m * BM;
+    rows = min(BM, cnt_cur - c_m * BM);
+  };
+  auto b_of = [&](int slot, int nt) {
+    const size_t b_row0 = (size_t)slot * NW + (SWIGLU ? nt * (BN / 2) : nt * BN);
+    return make_rsrc(B + b_row0 * K,
+                     (uint32_t)min((size_t)0x7fffffff, ((size_t)(slot + 1) * NW - b_row0) * K * 2));
+  };
+  auto a_of = [&](int row0, int rows) {
+    return GATHER ? make_rsrc(A, (uint32_t)A_rows * K * 2)
+                  : make_rsrc(A + (size_t)row0 * K, (uint32_t)rows * K * 2);
+  };
+  // Byte offsets of this lane's A chunks for a tile. GATHER: the wave's RW
+  // gathered rows come in by scalar loads (clamped to the tile's last row),
+  // pair index / kq by multiply-high with the host's magic number, and each
+  // lane picks its own; rows past the end read as zeros.
+  auto a_offsets = [&](int row0, int rows, int* a_off) {
+    int pv[RW];
+    if (GATHER) {
+#pragma unroll
+      for (int j = 0; j < RW; ++j) {
+        const uint32_t pj = (uint32_t)perm[row0 + min(wave * RW + j, rows - 1)];
+        pv[j] = (int)(kq_shift ? __umulhi(pj, kq_magic) >> (kq_shift - 1) : pj);
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < AI; ++i) {
+      const int r = wave * RW + i * RPI + lane / CH;
+      const int cc = ((lane % CH) ^ swz<CH>(r)) * 8;
+      if (GATHER) {
+        int t = pv[i * RPI];
+#pragma unroll
+        for (int j = 1; j < RPI; ++j) t = (lane / CH == j) ? pv[i * RPI + j] : t;
+        a_off[i] = (r < rows) ? (t * K + cc) * 2 : (int)0x80000000u;
+      } else {
+        a_off[i] = (r * K + cc) * 2;
+      }
+    }
+  };
+
+  int b_off[BI];
+#pragma unroll
+  for (int i = 0; i < BI; ++i) {
+    const int r = wave * (BN / NWAVE) + i * RPI + lane / CH;
+    const int wr = (SWIGLU && r >= BN / 2) ? I - BN / 2 + r : r;
+    b_off[i] = (wr * K + ((lane % CH) ^ swz<CH>(r)) * 8) * 2;
+  }
+  lds_u16* const smem3 = (lds_u16*)smem;
+  const int a_lds = wave * RW * BK;
+  const int b_lds = 2 * A_ST + wave * (BN / NWAVE) * BK;
+#define TG_ISSUE_A(rs, offs, k0, buf)                                                   \
+  do {                                                                                  \
+    _Pragma("unroll") for (int i = 0; i < AI; ++i)                                      \
+        load_lds16(rs, smem3 + (buf) * A_ST + a_lds + i * RPI * BK, offs[i], (k0) * 2); \
+  } while (0)
+#define TG_ISSUE_B(rs, k0, buf)                                                          \
+  do {                                                                                   \
+    _Pragma("unroll") for (int i = 0; i < BI; ++i)                                       \
+        load_lds16(rs, smem3 + (buf) * B_ST + b_lds + i * RPI * BK, b_off[i], (k0) * 2); \
+  } while (0)
+  const int khalf = lane >> 5;
+  const int xrow = wm * (BM / WM) + (lane & 31);
+  const int wrow = (SWIGLU ? wn * (BN / 2 / WN) : wn * (BN / WN)) + (lane & 31);
+  int xoff[BK / 16], woff[BK / 16];
+#pragma unroll
+  for (int kk = 0; kk < BK / 16; ++kk) {
+    xoff[kk] = xrow * BK + (((2 * kk + khalf) ^ swz<CH>(xrow)) << 3);
+    woff[kk] = 2 * A_ST + wrow * BK + (((2 * kk + khalf) ^ swz<CH>(wrow)) << 3);
+  }
+  auto wblk = [](int nb) constexpr {
+    return SWIGLU ? ((nb < NB / 2) ? nb * 32 : BN / 2 + (nb - NB / 2) * 32) : nb * 32;
+  };
+  const int nk = K / BK;  // at least 3 (checked by the launcher)
+  constexpr int KK = BK / 16;
+  static_assert(KK % 2 == 0, "fragment double buffering alternates within a stage");
+  bf16x8 xf[2][MB], wf[2][NB];
+  f32x16 acc[NB][MB];
+#define TG_FRAGS(abuf, bbuf, kk, dst)                                                       \
+  do {                                                                                      \
+    _Pragma("unroll") for (int mb = 0; mb < MB; ++mb) xf[dst][mb] =                         \
+        *reinterpret_cast<const bf16x8*>(smem + (abuf) * A_ST + xoff[kk] + mb * 32 * BK);   \
+    _Pragma("unroll") for (int nb = 0; nb < NB; ++nb) wf[dst][nb] =                         \
+        *reinterpret_cast<const bf16x8*>(smem + (bbuf) * B_ST + woff[kk] + wblk(nb) * BK);  \
+  } while (0)
+#define TG_MFMAS(src)                                                                       \
+  do {                                                                                      \
+    _Pragma("unroll") for (int nb = 0; nb < NB; ++nb)                                       \
+        _Pragma("unroll") for (int mb = 0; mb < MB; ++mb) acc[nb][mb] =                     \
+            __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[src][nb], xf[src][mb], acc[nb][mb],  \
+                                                    0, 0, 0);                               \
+  } while (0)
+  // Refill of the buffers of the stage just consumed: A of stage kt+2 and B
+  // of stage kt+3 of this tile, else of the next tile, else (no next tile)
+  // the last stage again into buffers nobody reads any more.
+#define TG_REFILL(kt)                                                                       \
+  do {                                                                                      \
+    const bool ca = (kt) + 2 < nk, cb = (kt) + 3 < nk;                                      \
+    const int ka = ca ? (kt) + 2 : (has_n ? (kt) + 2 - nk : nk - 1);                        \
+    const int kb = cb ? (kt) + 3 : (has_n ? (kt) + 3 - nk : nk - 1);                        \
+    if (ca || !has_n) TG_ISSUE_A(a_cur, a_off, ka * BK, ab);                                \
+    else TG_ISSUE_A(a_n, a_off_n, ka * BK, ab);                                             \
+    TG_ISSUE_B((cb || !has_n) ? b_cur : b_n, kb * BK, bb);                                  \
+  } while (0)
+
+  int slot, row0, rows, nt;
+  seek(L, slot, row0, rows, nt);
+  __amdgpu_buffer_rsrc_t a_cur = a_of(row0, rows), b_cur = b_of(slot, nt);
+  int a_off[AI], a_off_n[AI];
+  a_offsets(row0, rows, a_off);
+  int Ln = L + per_xcd_blocks;
+  bool has_n = Ln < hi;
+  int slot_n = slot, row0_n = row0, rows_n = rows, nt_n = nt;
+  if (has_n) seek(Ln, slot_n, row0_n, rows_n, nt_n);
+  __amdgpu_buffer_rsrc_t a_n = a_of(row0_n, rows_n), b_n = b_of(slot_n, nt_n);
+  a_offsets(row0_n, rows_n, a_off_n);
+
+  TG_ISSUE_A(a_cur, a_off, 0, 0);
+  TG_ISSUE_B(b_cur, 0, 0);
+  TG_ISSUE_B(b_cur, BK, 1);
+  TG_ISSUE_A(a_cur, a_off, BK, 1);
+  TG_ISSUE_B(b_cur, 2 * BK, 2);
+  TG_WAIT_VM(2 * BI + AI);
+  block_barrier();
+  TG_FRAGS(0, 0, 0, 0);
+
+  int ab = 0, bb = 0;  // buffers of the current stage (stages count on across tiles)
+  for (;;) {
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[nb][mb][r] = 0.0f;
+    const bool active = wm * (BM / WM) < rows;
+    if (active) {
+      for (int kt = 0; kt < nk; ++kt) {
+#pragma unroll
+        for (int kk = 0; kk < KK - 1; ++kk) {
+          TG_FRAGS(ab, bb, kk + 1, (kk + 1) & 1);
+          TG_MFMAS(kk & 1);
+        }
+        TG_WAIT_VM(BI);
+        __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)
+        block_barrier();
+        TG_REFILL(kt);
+        ab ^= 1;
+        bb = (bb == 2) ? 0 : bb + 1;
+        TG_FRAGS(ab, bb, 0, 0);
+        TG_MFMAS((KK - 1) & 1);
+      }
+    } else {
+      for (int kt = 0; kt < nk; ++kt) {
+        TG_WAIT_VM(BI);
+        block_barrier();
+        TG_REFILL(kt);
+        ab ^= 1;
+        bb = (bb == 2) ? 0 : bb + 1;
+      }
+      TG_FRAGS(ab, bb, 0, 0);
+    }
+    // acc[nb][mb] register r of lane l: row mb*32 + l%32, column
+    // nb*32 + 8*(r/4) + 4*(l/32) + r%4 of the wave's sub-tile.
+    if (active) {
+      const int colbase = SWIGLU ? nt * (BN / 2) + wn * WOUT : nt * BN + wn * WOUT;
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) {
+        const int r = wm * (BM / WM) + mb * 32 + (lane & 31);
+        uint16_t* crow = C + (size_t)(row0 + r) * ldc + colbase + 4 * (lane >> 5);
+#pragma unroll
+        for (int nb = 0; nb < (SWIGLU ? NB / 2 : NB); ++nb) {
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            float v[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              const int rr = 4 * q + e;
+              if (SWIGLU) {
+                const float g = acc[nb][mb][rr];
+                const float u = acc[nb + NB / 2][mb][rr];
+                v[e] = g / (1.0f + __expf(-g)) * u;
+              } else {
+                v[e] = acc[nb][mb][rr];
+              }
+            }
+            uint2 pk;
+            pk.x = pack_bf16x2(v[0], v[1]);
+            pk.y = pack_bf16x2(v[2], v[3]);
+            if (r < rows) *reinterpret_cast<uint2*>(crow + nb * 32 + 8 * q) = pk;
+          }
+        }
+      }
+    }
+    if (!has_n) break;
+    row0 = row0_n;
+    rows = rows_n;
+    nt = nt_n;
+    a_cur = a_n;
+    b_cur = b_n;
+#pragma unroll
+    for (int i = 0; i < AI; ++i) a_off[i] = a_off_n[i];
+    Ln += per_xcd_blocks;
+    has_n = Ln < hi;
+    if (has_n) {
+      seek(Ln, slot_n, row0_n, rows_n, nt_n);
+      a_n = a_of(row0_n, rows_n);
+      b_n = b_of(slot_n, nt_n);
+      a_offsets(row0_n, rows_n, a_off_n);
+    }
+  }
+  TG_WAIT_VM(0);  // no LDS write may land after the block ends
+#undef TG_REFILL
+#undef TG_FRAGS
+#undef TG_MFMAS
+#undef TG_ISSUE_A
+#undef TG_ISSUE_B
+}
+
 // One launch over all tiles. SPLIT: blocks below head_blocks take the
 // full-size tiles except the tail (kHead); the blocks after them take the
 // tail as quarter tiles, BM/2 x BN/2 with wave grid WMq x WNq (kTail). They
@@ -490,6 +773,24 @@ hipError_t launch_grouped(const uint16_t* A, const int32_t* offsets, int S, int 
   return hipGetLastError();
 }
 
+// Persistent launch: one block per CU (a multiple of 8), for K of at least 3
+// stages.
+template <int BM, int BN, int BK, int WM, int WN, bool SWIGLU, bool GATHER>
+hipError_t launch_persistent(const uint16_t* A, const int32_t* offsets, int S, const uint16_t* B,
+                             int K, int NW, int I, uint16_t* C, int ldc, int NT,
+                             hipStream_t stream, const int32_t* perm, int kq, int A_rows) {
+  // n / kq = mulhi(n, m) >> (l - 1) for every n < 2^31, with l = ceil(log2 kq)
+  // and m = ceil(2^(31 + l) / kq) < 2^32 (division by an invariant integer).
+  int l = 0;
+  while ((1 << l) < kq) ++l;
+  const uint32_t m = (uint32_t)((((uint64_t)1 << (31 + l)) + (uint64_t)kq - 1) / (uint64_t)kq);
+  const int grid = cu_count() / kXcds * kXcds;
+  hipLaunchKernelGGL((grouped_gemm_persistent_kernel<BM, BN, BK, WM, WN, SWIGLU, GATHER>),
+                     dim3(grid), dim3(64 * WM * WN), 0, stream, A, offsets, S, B, K, NW, I, C, ldc,
+                     NT, perm, m, l, A_rows);
+  return hipGetLastError();
+}
+
 // Tile shapes (BM, BN, BK, WM, WN) and quarter-tile wave grids (WMq, WNq).
 // Large: 256 x 256, 16 waves; the down projection runs its tail as 128 x 128
 // quarter tiles with the same 16 waves (the gate/up projection's quarter
@@ -510,8 +811,9 @@ hipError_t launch_ffn_gateup(const uint16_t* x_perm, const int32_t* offsets, int
   if (small_batch(S, max_rows))
     return launch_grouped<TG_SMALL, true, false, false>(x_perm, offsets, S, max_rows, w13, d,
                                                         2 * I, I, h, I, (2 * I) / kBN, stream);
-  return launch_grouped<TG_LARGE, true, false, false>(x_perm, offsets, S, max_rows, w13, d, 2 * I,
-                                                      I, h, I, (2 * I) / kBN, stream);
+  return launch_persistent<256, 256, 64, 4, 4, true, false>(x_perm, offsets, S, w13, d, 2 * I, I,
+                                                            h, I, (2 * I) / kBN, stream, nullptr, 1,
+                                                            0);
 }
 
 hipError_t launch_ffn_gateup_gather(const uint16_t* x, int T, const int32_t* perm, int k,
@@ -522,8 +824,8 @@ hipError_t launch_ffn_gateup_gather(const uint16_t* x, int T, const int32_t* per
   if (small_batch(S, max_rows))
     return launch_grouped<TG_SMALL, true, true, false>(x, offsets, S, max_rows, w13, d, 2 * I, I,
                                                        h, I, (2 * I) / kBN, stream, perm, k, T);
-  return launch_grouped<TG_LARGE, true, true, false>(x, offsets, S, max_rows, w13, d, 2 * I, I, h,
-                                                     I, (2 * I) / kBN, stream, perm, k, T);
+  return launch_persistent<256, 256, 64, 4, 4, true, true>(x, offsets, S, w13, d, 2 * I, I, h, I,
+                                                           (2 * I) / kBN, stream, perm, k, T);
 }
 
 hipError_t launch_ffn_down(const uint16_t* h, const int32_t* offsets, int S, int max_rows,
