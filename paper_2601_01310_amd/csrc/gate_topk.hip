@@ -2,8 +2,8 @@
 //
 // One wave per token at a time. In weight mode each lane accumulates its
 // stride of the hidden dimension in float64 for 8 experts at a time
-// (bf16*bf16 products are exact in float64), a butterfly reduction gives
-// every lane the full sums, and the float64 sum is rounded once to float32.
+// (bf16*bf16 products are exact in float64), a DPP reduction gives every
+// lane the full sums, and the float64 sum is rounded once to float32.
 // When the gate matrix fits (E*d*2 <= 96 KB) a block of 16 waves (16
 // tokens) stages it in LDS once, so the matrix is read from memory once per
 // 16 tokens instead of once per token. Top-k runs as k rounds of a wave
@@ -114,8 +114,35 @@ __device__ __forceinline__ void wave_topk_any(const float* lg, int E, int k, int
   else wave_topk<16>(lg, E, k, t, ids, w);
 }
 
+// Sum over the wave of a float64 held per lane, the same on every lane, in
+// a fixed order: DPP row steps (xor 1, xor 2, half-row mirror, row mirror)
+// give each 16-lane row its sum, then the four row sums are added.
+__device__ __forceinline__ double wave_sum_f64(double v) {
+#define TG_DPP_ADD(ctrl)                                                                     \
+  do {                                                                                       \
+    const int lo = __builtin_amdgcn_update_dpp(0, (int)__double2loint(v), ctrl, 0xF, 0xF,     \
+                                               false);                                       \
+    const int hi = __builtin_amdgcn_update_dpp(0, (int)__double2hiint(v), ctrl, 0xF, 0xF,     \
+                                               false);                                       \
+    v += __hiloint2double(hi, lo);                                                           \
+  } while (0)
+  TG_DPP_ADD(0xB1);
+  TG_DPP_ADD(0x4E);
+  TG_DPP_ADD(0x141);
+  TG_DPP_ADD(0x140);
+#undef TG_DPP_ADD
+  double total = 0.0;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int lo = __builtin_amdgcn_readlane((int)__double2loint(v), 16 * r);
+    const int hi = __builtin_amdgcn_readlane((int)__double2hiint(v), 16 * r);
+    total += __hiloint2double(hi, lo);
+  }
+  return total;
+}
+
 // float64 logits of token t for experts e0..e0+7 against a gate matrix
-// (global or LDS), written to lg by lane 0 after a butterfly reduction.
+// (global or LDS), written to lg by lane 0 after a wave reduction.
 template <typename WgPtr>
 __device__ __forceinline__ void logits8(const uint4* __restrict__ xr, WgPtr wg, int d, int E,
                                         int e0, float* lg) {
@@ -149,13 +176,8 @@ __device__ __forceinline__ void logits8(const uint4* __restrict__ xr, WgPtr wg, 
   }
 #pragma unroll
   for (int q = 0; q < 8; ++q) {
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) acc[q] += __shfl_xor(acc[q], off);
-  }
-  if (lane == 0) {
-#pragma unroll
-    for (int q = 0; q < 8; ++q)
-      if (e0 + q < E) lg[e0 + q] = (float)acc[q];
+    const double sum = wave_sum_f64(acc[q]);
+    if (lane == 0 && e0 + q < E) lg[e0 + q] = (float)sum;
   }
 }
 
