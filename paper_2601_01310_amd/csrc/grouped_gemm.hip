@@ -441,7 +441,8 @@ __device__ __forceinline__ void gemm_tile(uint16_t* smem, const TileInfo& tile,
 // (8-byte stores), so the epilogue needs no LDS and overlaps the next
 // tile's first loads. Same MFMA sequence per output element as
 // grouped_gemm_kernel, hence the same bits.
-template <int BM, int BN, int BK, int WM, int WN, bool SWIGLU, bool GATHER>
+template <int BM, int BN, int BK, int WM, int WN, bool SWIGLU, bool GATHER, bool TAIL = false,
+          int WMq = WM, int WNq = WN>
 __global__ __launch_bounds__(64 * WM * WN) void grouped_gemm_persistent_kernel(
     const uint16_t* __restrict__ A, const int32_t* __restrict__ offsets, int S,
     const uint16_t* __restrict__ B, int K, int NW, int I, uint16_t* __restrict__ C, int ldc,
@@ -458,15 +459,22 @@ __global__ __launch_bounds__(64 * WM * WN) void grouped_gemm_persistent_kernel(
   constexpr int WOUT = SWIGLU ? BN / 2 / WN : BN / WN;
   static_assert(MB >= 1 && NB >= 1 && AI >= 1 && BI >= 1 && (BK == 32 || BK == 64), "tile");
   static_assert(!SWIGLU || NB % 2 == 0, "gate/up halves");
+  static_assert(!(TAIL && GATHER), "quarter tiles read pre-permuted rows");
   __shared__ __attribute__((aligned(16))) uint16_t smem[2 * A_ST + 3 * B_ST];
 
   const int total = count_tiles(offsets, S, BM, NT);
   const int per_xcd_blocks = gridDim.x / kXcds;
   const int x = blockIdx.x % kXcds, c = blockIdx.x / kXcds;
-  const int per = (total + kXcds - 1) / kXcds;
-  const int lo = x * per, hi = min(lo + per, total);
+  // TAIL: when the tiles past the last full round (one block per CU) would
+  // occupy at most half of the CUs, they are left out of the walk and run
+  // afterwards as quarter tiles.
+  const int rem = TAIL ? total % (int)gridDim.x : 0;
+  const bool tail = rem > 0 && 2 * rem <= (int)gridDim.x;
+  const int n_head = tail ? total - rem : total;
+  const int per = (n_head + kXcds - 1) / kXcds;
+  const int lo = x * per, hi = min(lo + per, n_head);
   int L = lo + c;
-  if (L >= hi) return;
+  if (L < hi) {
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -706,12 +714,38 @@ __global__ __launch_bounds__(64 * WM * WN) void grouped_gemm_persistent_kernel(
       a_offsets(row0_n, rows_n, a_off_n);
     }
   }
-  TG_WAIT_VM(0);  // no LDS write may land after the block ends
+  TG_WAIT_VM(0);  // no LDS write may land after the walk
 #undef TG_REFILL
 #undef TG_FRAGS
 #undef TG_MFMAS
 #undef TG_ISSUE_A
 #undef TG_ISSUE_B
+  }
+  if constexpr (TAIL) {
+    if (!tail) return;
+    // Quarter q of the tail: tile n_head + q / 4, row half (q % 4) / 2,
+    // column half q % 2; the XCD's share of the quarters, one at a time
+    // (each with its own pipeline and LDS epilogue).
+    __syncthreads();
+    const int nq = 4 * rem;
+    const int qper = (nq + kXcds - 1) / kXcds;
+    const int qhi = min(x * qper + qper, nq);
+    for (int q = x * qper + c; q < qhi; q += per_xcd_blocks) {
+      TileInfo t;
+      int m;
+      if (!find_tile(offsets, S, BM, NT, n_head + q / 4, &t, &m)) break;
+      m = 2 * m + (q % 4) / 2;
+      t.nt = 2 * t.nt + q % 2;
+      const int rows = min(BM / 2, t.rows - m * (BM / 2));
+      if (rows > 0) {
+        t.row0 += m * (BM / 2);
+        t.rows = rows;
+        gemm_tile<BM / 2, BN / 2, BK, WMq, WNq, SWIGLU, GATHER>(smem, t, A, B, K, NW, I, C, ldc,
+                                                                perm, 1, A_rows);
+        __syncthreads();
+      }
+    }
+  }
 }
 
 // One launch over all tiles. SPLIT: blocks below head_blocks take the
@@ -775,7 +809,8 @@ hipError_t launch_grouped(const uint16_t* A, const int32_t* offsets, int S, int 
 
 // Persistent launch: one block per CU (a multiple of 8), for K of at least 3
 // stages.
-template <int BM, int BN, int BK, int WM, int WN, bool SWIGLU, bool GATHER>
+template <int BM, int BN, int BK, int WM, int WN, bool SWIGLU, bool GATHER, bool TAIL = false,
+          int WMq = WM, int WNq = WN>
 hipError_t launch_persistent(const uint16_t* A, const int32_t* offsets, int S, const uint16_t* B,
                              int K, int NW, int I, uint16_t* C, int ldc, int NT,
                              hipStream_t stream, const int32_t* perm, int kq, int A_rows) {
@@ -785,9 +820,10 @@ hipError_t launch_persistent(const uint16_t* A, const int32_t* offsets, int S, c
   while ((1 << l) < kq) ++l;
   const uint32_t m = (uint32_t)((((uint64_t)1 << (31 + l)) + (uint64_t)kq - 1) / (uint64_t)kq);
   const int grid = cu_count() / kXcds * kXcds;
-  hipLaunchKernelGGL((grouped_gemm_persistent_kernel<BM, BN, BK, WM, WN, SWIGLU, GATHER>),
-                     dim3(grid), dim3(64 * WM * WN), 0, stream, A, offsets, S, B, K, NW, I, C, ldc,
-                     NT, perm, m, l, A_rows);
+  hipLaunchKernelGGL(
+      (grouped_gemm_persistent_kernel<BM, BN, BK, WM, WN, SWIGLU, GATHER, TAIL, WMq, WNq>),
+      dim3(grid), dim3(64 * WM * WN), 0, stream, A, offsets, S, B, K, NW, I, C, ldc, NT, perm, m,
+      l, A_rows);
   return hipGetLastError();
 }
 
@@ -834,8 +870,8 @@ hipError_t launch_ffn_down(const uint16_t* h, const int32_t* offsets, int S, int
   if (small_batch(S, max_rows))
     return launch_grouped<TG_SMALL, false, false, false>(h, offsets, S, max_rows, w2, I, d, 0, y,
                                                          d, d / kBN, stream);
-  return launch_grouped<TG_LARGE, false, false, true>(h, offsets, S, max_rows, w2, I, d, 0, y, d,
-                                                      d / kBN, stream);
+  return launch_persistent<256, 256, 64, 4, 4, false, false, true, 4, 4>(
+      h, offsets, S, w2, I, d, 0, y, d, d / kBN, stream, nullptr, 1, 0);
 }
 
 hipError_t launch_expert_ffn(const uint16_t* x_perm, const int32_t* offsets, int S, int max_rows,
