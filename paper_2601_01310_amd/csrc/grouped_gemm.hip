@@ -33,14 +33,15 @@
 // and written as 16-byte row segments.
 //
 // Tile shapes: 256 x 256 with 16 waves for batches that fill the MFMA
-// units, and 32 x 256 with 4 waves (104 KB of LDS) for small per-slot
-// batches, where the launch only streams weights and a 256-row tile would
-// stage and multiply mostly zero rows. The host picks between the two from
-// the row bound alone (mean rows per slot at most 32), never from the device
-// counts. In the down projection with 256 x 256 tiles, a partial last round
-// that would leave at least half of the CUs idle is run as 128 x 128
-// quarter tiles by blocks appended to the same launch. All shapes give
-// identical bits.
+// units, run by a persistent kernel (one block per CU walking its tiles with
+// the DMA pipeline running on across tiles); and 32 x 256 with 4 waves
+// (104 KB of LDS), one block per tile, for small per-slot batches, where the
+// launch only streams weights and a 256-row tile would stage and multiply
+// mostly zero rows. The host picks between the two from the row bound alone
+// (mean rows per slot at most 32), never from the device counts. In the down
+// projection, a partial last round of 256 x 256 tiles that would leave at
+// least half of the CUs idle is run afterwards as 128 x 128 quarter tiles by
+// the same blocks. All shapes give identical bits.
 //
 // Tile order: the tiles of one launch are enumerated slot by slot, then by
 // weight panel (n), then by row block (m), so consecutive tiles share a
@@ -96,18 +97,6 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, ui
 struct TileInfo {
   int slot, row0, rows, nt;
 };
-
-// Which tiles a block takes. kAll: every tile. kHead: every tile but the
-// tail, when there is one. kTail: the tail only, each tile of the tail split
-// into SM x SN sub-tiles (SM row blocks, SN column panels; the block's own BM
-// and NT are those of the sub-tiles).
-//
-// The tail is the partial last round of a launch whose tile count is not a
-// multiple of the CU count; when it would occupy at most half of the CUs,
-// its tiles are run as SM * SN times as many sub-tiles, so that the last
-// round keeps more CUs busy. Every output element is the same MFMA
-// accumulation sequence whatever the tile shape, so the split changes no bit.
-enum TileMode { kAll = 0, kHead = 1, kTail = 2 };
 
 // Number of tiles of BMx rows x NTx panels over all slots (every lane gets
 // the sum).
@@ -170,34 +159,16 @@ __device__ __forceinline__ bool find_tile(const int32_t* __restrict__ offsets, i
 // Blocks are dealt to the XCDs round robin; block b takes logical tile
 // (b % 8) * (R / 8) + b / 8, so each XCD works through one contiguous range.
 // Returns false (uniformly) when the block has no tile.
-template <int BM, int MODE, int SM = 1, int SN = 1>
-__device__ __forceinline__ bool map_tile(const int32_t* __restrict__ offsets, int S, int NT,
-                                         int ncu, int b, TileInfo* t) {
-  const int BMb = (MODE == kTail) ? BM * SM : BM;  // tiles counted at the full size
-  const int NTb = (MODE == kTail) ? NT / SN : NT;
-  const int total = count_tiles(offsets, S, BMb, NTb);
-  const int rem = (MODE == kAll) ? 0 : total % ncu;
-  const bool tail = rem > 0 && 2 * rem <= ncu;
-  int n_here;
-  if (MODE == kTail) {
-    if (!tail) return false;
-    n_here = SM * SN * rem;
-  } else {
-    n_here = tail ? total - rem : total;
-  }
-  const int R = (n_here + kXcds - 1) / kXcds * kXcds;
+template <int BM>
+__device__ __forceinline__ bool map_tile(const int32_t* __restrict__ offsets, int S, int NT, int b,
+                                         TileInfo* t) {
+  const int total = count_tiles(offsets, S, BM, NT);
+  const int R = (total + kXcds - 1) / kXcds * kXcds;
   if (b >= R) return false;
   const int L = (b % kXcds) * (R / kXcds) + b / kXcds;
-  if (L >= n_here) return false;
+  if (L >= total) return false;
   int m;
-  if (MODE != kTail) {
-    if (!find_tile(offsets, S, BM, NT, L, t, &m)) return false;
-  } else {
-    if (!find_tile(offsets, S, BMb, NTb, total - rem + L / (SM * SN), t, &m)) return false;
-    const int q = L % (SM * SN);
-    m = SM * m + q / SN;
-    t->nt = SN * t->nt + q % SN;
-  }
+  if (!find_tile(offsets, S, BM, NT, L, t, &m)) return false;
   const int rows = min(BM, t->rows - m * BM);
   if (rows <= 0) return false;
   t->row0 += m * BM;
@@ -748,35 +719,17 @@ __global__ __launch_bounds__(64 * WM * WN) void grouped_gemm_persistent_kernel(
   }
 }
 
-// One launch over all tiles. SPLIT: blocks below head_blocks take the
-// full-size tiles except the tail (kHead); the blocks after them take the
-// tail as quarter tiles, BM/2 x BN/2 with wave grid WMq x WNq (kTail). They
-// are dispatched last, so they fill the CUs that the last round of full
-// tiles leaves idle.
-template <int BM, int BN, int BK, int WM, int WN, int WMq, int WNq, bool SWIGLU, bool GATHER,
-          bool SPLIT>
+// One block per tile (the small-batch shape).
+template <int BM, int BN, int BK, int WM, int WN, bool SWIGLU, bool GATHER>
 __global__ __launch_bounds__(64 * WM * WN) void grouped_gemm_kernel(
     const uint16_t* __restrict__ A, const int32_t* __restrict__ offsets, int S,
     const uint16_t* __restrict__ B, int K, int NW, int I, uint16_t* __restrict__ C, int ldc,
-    int NT, const int32_t* __restrict__ perm, int kq, int A_rows, int ncu, int head_blocks) {
-  static_assert(WMq * WNq == WM * WN, "quarter tiles use the block's waves");
+    int NT, const int32_t* __restrict__ perm, int kq, int A_rows) {
   __shared__ __attribute__((aligned(16))) uint16_t smem[2 * BM * BK + 3 * BN * BK];
   TileInfo tile;
-  const int b = blockIdx.x;
-  if constexpr (!SPLIT) {
-    if (map_tile<BM, kAll>(offsets, S, NT, ncu, b, &tile))
-      gemm_tile<BM, BN, BK, WM, WN, SWIGLU, GATHER>(smem, tile, A, B, K, NW, I, C, ldc, perm, kq,
-                                                    A_rows);
-  } else {
-    if (b < head_blocks) {
-      if (map_tile<BM, kHead, 2, 2>(offsets, S, NT, ncu, b, &tile))
-        gemm_tile<BM, BN, BK, WM, WN, SWIGLU, GATHER>(smem, tile, A, B, K, NW, I, C, ldc, perm, kq,
-                                                      A_rows);
-    } else if (map_tile<BM / 2, kTail, 2, 2>(offsets, S, 2 * NT, ncu, b - head_blocks, &tile)) {
-      gemm_tile<BM / 2, BN / 2, BK, WMq, WNq, SWIGLU, GATHER>(smem, tile, A, B, K, NW, I, C, ldc,
-                                                              perm, kq, A_rows);
-    }
-  }
+  if (map_tile<BM>(offsets, S, NT, blockIdx.x, &tile))
+    gemm_tile<BM, BN, BK, WM, WN, SWIGLU, GATHER>(smem, tile, A, B, K, NW, I, C, ldc, perm, kq,
+                                                  A_rows);
 }
 
 int cu_count() {
@@ -787,23 +740,18 @@ int cu_count() {
   return n;
 }
 
-template <int BM, int BN, int BK, int WM, int WN, int WMq, int WNq, bool SWIGLU, bool GATHER,
-          bool SPLIT>
+template <int BM, int BN, int BK, int WM, int WN, bool SWIGLU, bool GATHER>
 hipError_t launch_grouped(const uint16_t* A, const int32_t* offsets, int S, int max_rows,
                           const uint16_t* B, int K, int NW, int I, uint16_t* C, int ldc, int NT,
                           hipStream_t stream, const int32_t* perm = nullptr, int kq = 1,
                           int A_rows = 0) {
   // Bound on the tile count: sum_s ceil(count_s / BM) <= ceil(max_rows / BM) + S.
   const long bound = ((long)(max_rows + BM - 1) / BM + S) * NT;
-  const long head = (bound + kXcds - 1) / kXcds * kXcds;
-  const int ncu = SPLIT ? cu_count() : 1;
-  // A tail holds at most ncu / 2 tiles, hence at most 2 * ncu quarters.
-  const long tail = SPLIT ? (2L * ncu + kXcds - 1) / kXcds * kXcds : 0;
-  if (head == 0) return hipSuccess;
-  hipLaunchKernelGGL(
-      (grouped_gemm_kernel<BM, BN, BK, WM, WN, WMq, WNq, SWIGLU, GATHER, SPLIT>),
-      dim3((unsigned)(head + tail)), dim3(64 * WM * WN), 0, stream, A, offsets, S, B, K, NW, I, C,
-      ldc, NT, perm, kq, A_rows, ncu, (int)head);
+  const long grid = (bound + kXcds - 1) / kXcds * kXcds;
+  if (grid == 0) return hipSuccess;
+  hipLaunchKernelGGL((grouped_gemm_kernel<BM, BN, BK, WM, WN, SWIGLU, GATHER>),
+                     dim3((unsigned)grid), dim3(64 * WM * WN), 0, stream, A, offsets, S, B, K, NW,
+                     I, C, ldc, NT, perm, kq, A_rows);
   return hipGetLastError();
 }
 
@@ -827,13 +775,13 @@ hipError_t launch_persistent(const uint16_t* A, const int32_t* offsets, int S, c
   return hipGetLastError();
 }
 
-// Tile shapes (BM, BN, BK, WM, WN) and quarter-tile wave grids (WMq, WNq).
+// Small-batch tile shape (BM, BN, BK, WM, WN); the full-size shape is
+// 256 x 256 x 64 with 4 x 4 waves (persistent kernel).
 // Large: 256 x 256, 16 waves; the down projection runs its tail as 128 x 128
 // quarter tiles with the same 16 waves (the gate/up projection's quarter
 // tiles would need an even number of 32-column blocks per wave, hence at most
 // 8 waves, so it runs its tail at full size). Small: 32 x 256, 4 waves.
-#define TG_LARGE 256, 256, 64, 4, 4, 4, 4
-#define TG_SMALL 32, 256, 64, 1, 4, 1, 4
+#define TG_SMALL 32, 256, 64, 1, 4
 constexpr int kBN = 256;
 constexpr int kSmallRowsPerSlot = 32;
 
@@ -845,7 +793,7 @@ hipError_t launch_ffn_gateup(const uint16_t* x_perm, const int32_t* offsets, int
                              const uint16_t* w13, int d, int I, uint16_t* h, hipStream_t stream) {
   if (max_rows == 0) return hipSuccess;
   if (small_batch(S, max_rows))
-    return launch_grouped<TG_SMALL, true, false, false>(x_perm, offsets, S, max_rows, w13, d,
+    return launch_grouped<TG_SMALL, true, false>(x_perm, offsets, S, max_rows, w13, d,
                                                         2 * I, I, h, I, (2 * I) / kBN, stream);
   return launch_persistent<256, 256, 64, 4, 4, true, false>(x_perm, offsets, S, w13, d, 2 * I, I,
                                                             h, I, (2 * I) / kBN, stream, nullptr, 1,
@@ -858,7 +806,7 @@ hipError_t launch_ffn_gateup_gather(const uint16_t* x, int T, const int32_t* per
                                     hipStream_t stream) {
   if (max_rows == 0) return hipSuccess;
   if (small_batch(S, max_rows))
-    return launch_grouped<TG_SMALL, true, true, false>(x, offsets, S, max_rows, w13, d, 2 * I, I,
+    return launch_grouped<TG_SMALL, true, true>(x, offsets, S, max_rows, w13, d, 2 * I, I,
                                                        h, I, (2 * I) / kBN, stream, perm, k, T);
   return launch_persistent<256, 256, 64, 4, 4, true, true>(x, offsets, S, w13, d, 2 * I, I, h, I,
                                                            (2 * I) / kBN, stream, perm, k, T);
@@ -868,7 +816,7 @@ hipError_t launch_ffn_down(const uint16_t* h, const int32_t* offsets, int S, int
                            const uint16_t* w2, int d, int I, uint16_t* y, hipStream_t stream) {
   if (max_rows == 0) return hipSuccess;
   if (small_batch(S, max_rows))
-    return launch_grouped<TG_SMALL, false, false, false>(h, offsets, S, max_rows, w2, I, d, 0, y,
+    return launch_grouped<TG_SMALL, false, false>(h, offsets, S, max_rows, w2, I, d, 0, y,
                                                          d, d / kBN, stream);
   return launch_persistent<256, 256, 64, 4, 4, false, false, true, 4, 4>(
       h, offsets, S, w2, I, d, 0, y, d, d / kBN, stream, nullptr, 1, 0);
