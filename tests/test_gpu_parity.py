@@ -153,6 +153,41 @@ def test_ffn_partial_last_round_split_matches_oracle():
     assert np.array_equal(Y[:n], ys[1][1]), "rows differ between layouts with and without a spill"
 
 
+def test_persistent_walk_matches_small_tiles_bitwise():
+    """Forty slots, every other one empty, with row counts around the tile
+    edges (1, 31, 32, 33, 255, 256, 257, ...): with max_rows at most 32 per
+    slot the 32-row kernel runs, one block per tile; above it the persistent
+    kernel walks 320 gate/up tiles over the CUs (more than one per block,
+    across the empty slots) and runs all of the down GEMM's tiles as tail
+    quarters. Both must give the same bits, and the oracle's values."""
+    d, I, S = 1024, 2560, 40
+    base = [0, 1, 31, 32, 33, 255, 256, 257, 0, 0, 2, 63, 64, 65, 100, 0, 17, 5, 1, 0]
+    counts = [c for b in base for c in (b, 0)]
+    P = sum(counts)
+    assert len(counts) == S and P <= 32 * S
+    assert sum((c + 255) // 256 for c in counts) * (2 * I // 256) == 320
+    big = 32 * S + 1
+    g = torch.Generator().manual_seed(21)
+    x = torch.randn((big, d), generator=g).to(torch.bfloat16).to(DEV)
+    w13 = (torch.randn((S, 2 * I, d), generator=g) * 0.02).to(torch.bfloat16).to(DEV)
+    w2 = (torch.randn((S, d, I), generator=g) * 0.02).to(torch.bfloat16).to(DEV)
+    off = np.concatenate([[0], np.cumsum(counts)]).astype(np.int32)
+    offd = torch.from_numpy(off).to(DEV)
+    res = []
+    for max_rows in (P, big):
+        h = torch.zeros((big, I), dtype=torch.bfloat16, device=DEV)
+        y = torch.zeros((big, d), dtype=torch.bfloat16, device=DEV)
+        tg.tg_expert_ffn_grouped(x, offd, S, max_rows, w13, w2, d, I, h, y)
+        torch.cuda.synchronize()
+        res.append((u16(h[:P]), u16(y[:P])))
+    assert np.array_equal(res[0][0], res[1][0]), "h: persistent vs 32-row tiles"
+    assert np.array_equal(res[0][1], res[1][1]), "y: persistent vs 32-row tiles"
+    for s_ in (10, 12, 14, 28):
+        a, b = int(off[s_]), int(off[s_ + 1])
+        ref = O.expert_ffn(u16(x[a:b]), u16(w13[s_]), u16(w2[s_]))[1]
+        G.assert_close_bf16(res[1][1][a:b], ref, f"y slot {s_}")
+
+
 def test_repeat_calls_are_bit_identical(tiny):
     a, b = G.run_fused(tiny), G.run_fused(tiny)
     for key in a:
@@ -193,6 +228,9 @@ def test_random_shapes_match_oracle(case):
         G.assert_close_bf16(g["h"], r["h"], "h")
         G.assert_close_bf16(g["y"], r["y"], "y")
         G.assert_close_bf16(g["out"], r["out"], "out")
+        # the fused forward reads token rows in place (gathered); same bits
+        f = G.run_fused(wl, al)
+        assert np.array_equal(f["out"], g["out"]), "fused differs from stepwise"
 
 
 def test_empty_batch():
