@@ -29,19 +29,21 @@
 // For GEMM1 the weight tile holds BN/2 gate rows and the matching BN/2 up
 // rows and every wave owns equal numbers of both, so g and u of one output
 // element land in the same lane and register and the SwiGLU epilogue needs
-// no data exchange. Results are staged through each wave's own LDS region
-// and written as 16-byte row segments.
+// no data exchange.
 //
-// Tile shapes: 256 x 256 with 16 waves for batches that fill the MFMA
-// units, run by a persistent kernel (one block per CU walking its tiles with
-// the DMA pipeline running on across tiles); and 32 x 256 with 4 waves
-// (104 KB of LDS), one block per tile, for small per-slot batches, where the
-// launch only streams weights and a 256-row tile would stage and multiply
-// mostly zero rows. The host picks between the two from the row bound alone
-// (mean rows per slot at most 32), never from the device counts. In the down
-// projection, a partial last round of 256 x 256 tiles that would leave at
-// least half of the CUs idle is run afterwards as 128 x 128 quarter tiles by
-// the same blocks. All shapes give identical bits.
+// Tile shapes: 256 x 256 with 4 waves (one per SIMD, 128 x 128 each) for
+// batches that fill the MFMA units, run by a persistent kernel (one block
+// per CU walking its tiles with the DMA pipeline running on across tiles,
+// results written straight from the accumulators); and 32 x 256 with 4
+// waves (104 KB of LDS), one block per tile, for small per-slot batches,
+// where the launch only streams weights and a 256-row tile would stage and
+// multiply mostly zero rows (results staged through each wave's own LDS
+// region and written as 16-byte row segments). The host picks between the
+// two from the row bound alone (mean rows per slot at most 32), never from
+// the device counts. In the down projection, a partial last round of
+// 256 x 256 tiles that would leave at least half of the CUs idle is run
+// afterwards as 128 x 128 quarter tiles by the same blocks. All shapes give
+// identical bits.
 //
 // Tile order: the tiles of one launch are enumerated slot by slot, then by
 // weight panel (n), then by row block (m), so consecutive tiles share a
@@ -78,6 +80,14 @@ __device__ __forceinline__ void block_barrier() {
 }
 
 typedef __attribute__((address_space(3))) uint16_t lds_u16;
+
+// SwiGLU of one output element: silu(g) * u = g / (1 + e^-g) * u, with the
+// reciprocal from the hardware approximation (about 1 ulp in float32, far
+// below the bf16 rounding of h). Every kernel's epilogue uses this one
+// expression, so all tile shapes give the same bits.
+__device__ __forceinline__ float swiglu(float g, float u) {
+  return g * __builtin_amdgcn_rcpf(1.0f + __expf(-g)) * u;
+}
 
 // One 16-byte global -> LDS transfer per lane; the wave's 64 chunks land at
 // consecutive 16-byte positions starting at the (wave-uniform) `lds` row.
@@ -371,7 +381,7 @@ __device__ __forceinline__ void gemm_tile(uint16_t* smem, const TileInfo& tile,
           if (SWIGLU) {
             const float g = acc[nb][mb][r];
             const float u = acc[nb + NB / 2][mb][r];
-            v[e] = g / (1.0f + __expf(-g)) * u;
+            v[e] = swiglu(g, u);
           } else {
             v[e] = acc[nb][mb][r];
           }
@@ -402,43 +412,45 @@ __device__ __forceinline__ void gemm_tile(uint16_t* smem, const TileInfo& tile,
   }
 }
 
-// Persistent variant for the gate/up projection with full-size tiles: one
-// block per CU, each walking the tiles of its XCD's contiguous range with a
-// stride of the XCD's block count. The DMA pipeline runs on across tiles:
-// the last stages of one tile issue the first stages of the next, whose
-// slot, rows and (when GATHER) gathered row offsets are found ahead of time
-// with scalar loads, which do not disturb the vector-memory counts that the
-// pipeline waits on. Results go straight from the accumulators to memory
-// (8-byte stores), so the epilogue needs no LDS and overlaps the next
-// tile's first loads. Same MFMA sequence per output element as
-// grouped_gemm_kernel, hence the same bits.
-template <int BM, int BN, int BK, int WM, int WN, bool SWIGLU, bool GATHER, bool TAIL = false,
-          int WMq = WM, int WNq = WN>
-__global__ __launch_bounds__(64 * WM * WN) void grouped_gemm_persistent_kernel(
+// Persistent kernel with one wave per SIMD: 4 waves (2 x 2), each computing
+// 128 x 128 of the 256 x 256 tile, so each fragment read from LDS feeds four
+// MFMAs instead of two. That halves the LDS read traffic of the 16-wave
+// shape, and under the power limit the clock stays higher. With a single
+// wave per SIMD no other wave covers a gap in the instruction stream, so the
+// order within a stage of four k16 sub-steps is fixed explicitly:
+//   sub-steps 0-2: 16 MFMAs with the next sub-step's fragment reads and a
+//               quarter of the stage's DMA loads among them (A in sub-steps
+//               0 and 1, B in sub-step 2);
+//   sub-step 3: 8 MFMAs with the last quarter of the loads, then the wait
+//               and the block barrier while they run, then the next stage's
+//               first fragments interleaved with the other 8 MFMAs.
+// During stage g (counted on across tiles) A of stage g+1 and B of stage g+2
+// are loaded into the buffers that stage g-1 released at the previous
+// barrier; at the end of stage g only B of stage g+2 may still be in flight.
+// Loads past the last stage of the walk re-load that stage into released
+// buffers, so every wait counts the same number of loads. Same MFMA sequence
+// per output element as the other kernels, hence the same bits.
+template <bool SWIGLU, bool GATHER, bool TAIL>
+__global__ __launch_bounds__(256) void grouped_gemm_persistent4_kernel(
     const uint16_t* __restrict__ A, const int32_t* __restrict__ offsets, int S,
     const uint16_t* __restrict__ B, int K, int NW, int I, uint16_t* __restrict__ C, int ldc,
     int NT, const int32_t* __restrict__ perm, uint32_t kq_magic, int kq_shift, int A_rows) {
-  constexpr int NWAVE = WM * WN;
-  constexpr int MB = BM / WM / 32;
-  constexpr int NB = BN / WN / 32;
-  constexpr int CH = BK / 8;
-  constexpr int RPI = 64 / CH;
-  constexpr int RW = BM / NWAVE;            // staged A rows per wave
-  constexpr int AI = RW / RPI;
-  constexpr int BI = BN / NWAVE / RPI;
+  constexpr int BM = 256, BN = 256, BK = 64, WM = 2, WN = 2, NWAVE = WM * WN;
+  constexpr int MB = BM / WM / 32, NB = BN / WN / 32;  // 4 x 4 blocks of 32 x 32 per wave
+  constexpr int CH = BK / 8;                            // 16-byte chunks per staged row
+  constexpr int RPI = 64 / CH;                          // staged rows per load instruction
+  constexpr int RW = BM / NWAVE;                        // staged A rows per wave
+  constexpr int AI = RW / RPI, BI = BN / NWAVE / RPI;   // load instructions per stage
   constexpr int A_ST = BM * BK, B_ST = BN * BK;
   constexpr int WOUT = SWIGLU ? BN / 2 / WN : BN / WN;
-  static_assert(MB >= 1 && NB >= 1 && AI >= 1 && BI >= 1 && (BK == 32 || BK == 64), "tile");
-  static_assert(!SWIGLU || NB % 2 == 0, "gate/up halves");
+  constexpr int KK = BK / 16;
+  static_assert(KK == 4 && AI == 8 && BI == 8 && MB * NB == 16, "schedule assumes this shape");
   static_assert(!(TAIL && GATHER), "quarter tiles read pre-permuted rows");
   __shared__ __attribute__((aligned(16))) uint16_t smem[2 * A_ST + 3 * B_ST];
 
   const int total = count_tiles(offsets, S, BM, NT);
   const int per_xcd_blocks = gridDim.x / kXcds;
   const int x = blockIdx.x % kXcds, c = blockIdx.x / kXcds;
-  // TAIL: when the tiles past the last full round (one block per CU) would
-  // occupy at most half of the CUs, they are left out of the walk and run
-  // afterwards as quarter tiles.
   const int rem = TAIL ? total % (int)gridDim.x : 0;
   const bool tail = rem > 0 && 2 * rem <= (int)gridDim.x;
   const int n_head = tail ? total - rem : total;
@@ -446,247 +458,295 @@ __global__ __launch_bounds__(64 * WM * WN) void grouped_gemm_persistent_kernel(
   const int lo = x * per, hi = min(lo + per, n_head);
   int L = lo + c;
   if (L < hi) {
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm = wave / WN, wn = wave % WN;
 
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wave / WN, wn = wave % WN;
-
-  // Scalar cursor over the slots and over (panel, row block) within the
-  // slot; a block's tiles come in increasing order, at most one stride
-  // apart, so the cursor only moves forward, and no step divides (a
-  // division would borrow vector registers that in-flight loads still
-  // address).
-  int s_cur = 0, before = 0, pos = 0, c_nt = 0, c_m = 0;
-  int o_cur = offsets[0];
-  int cnt_cur = offsets[1] - o_cur;
-  int mt_cur = (cnt_cur + BM - 1) / BM;
-  auto seek = [&](int Lq, int& slot, int& row0, int& rows, int& nt) {
-    while (Lq >= before + mt_cur * NT) {
-      before += mt_cur * NT;
-      ++s_cur;
-      o_cur = offsets[s_cur];
-      cnt_cur = offsets[s_cur + 1] - o_cur;
-      mt_cur = (cnt_cur + BM - 1) / BM;
-      pos = before;
-      c_nt = 0;
-      c_m = 0;
-    }
-    for (c_m += Lq - pos; c_m >= mt_cur; c_m -= mt_cur) ++c_nt;
-    pos = Lq;
-    slot = s_cur;
-    nt = c_nt;
-    row0 = o_cur + c_m * BM;
-    rows = min(BM, cnt_cur - c_m * BM);
-  };
-  auto b_of = [&](int slot, int nt) {
-    const size_t b_row0 = (size_t)slot * NW + (SWIGLU ? nt * (BN / 2) : nt * BN);
-    return make_rsrc(B + b_row0 * K,
-                     (uint32_t)min((size_t)0x7fffffff, ((size_t)(slot + 1) * NW - b_row0) * K * 2));
-  };
-  auto a_of = [&](int row0, int rows) {
-    return GATHER ? make_rsrc(A, (uint32_t)A_rows * K * 2)
-                  : make_rsrc(A + (size_t)row0 * K, (uint32_t)rows * K * 2);
-  };
-  // Byte offsets of this lane's A chunks for a tile. GATHER: the wave's RW
-  // gathered rows come in by scalar loads (clamped to the tile's last row),
-  // pair index / kq by multiply-high with the host's magic number, and each
-  // lane picks its own; rows past the end read as zeros.
-  auto a_offsets = [&](int row0, int rows, int* a_off) {
-    int pv[RW];
-    if (GATHER) {
-#pragma unroll
-      for (int j = 0; j < RW; ++j) {
-        const uint32_t pj = (uint32_t)perm[row0 + min(wave * RW + j, rows - 1)];
-        pv[j] = (int)(kq_shift ? __umulhi(pj, kq_magic) >> (kq_shift - 1) : pj);
+    int s_cur = 0, before = 0, pos = 0, c_nt = 0, c_m = 0;
+    int o_cur = offsets[0];
+    int cnt_cur = offsets[1] - o_cur;
+    int mt_cur = (cnt_cur + BM - 1) / BM;
+    auto seek = [&](int Lq, int& slot, int& row0, int& rows, int& nt) {
+      while (Lq >= before + mt_cur * NT) {
+        before += mt_cur * NT;
+        ++s_cur;
+        o_cur = offsets[s_cur];
+        cnt_cur = offsets[s_cur + 1] - o_cur;
+        mt_cur = (cnt_cur + BM - 1) / BM;
+        pos = before;
+        c_nt = 0;
+        c_m = 0;
       }
-    }
+      for (c_m += Lq - pos; c_m >= mt_cur; c_m -= mt_cur) ++c_nt;
+      pos = Lq;
+      slot = s_cur;
+      nt = c_nt;
+      row0 = o_cur + c_m * BM;
+      rows = min(BM, cnt_cur - c_m * BM);
+    };
+    auto b_of = [&](int slot, int nt) {
+      const size_t b_row0 = (size_t)slot * NW + (SWIGLU ? nt * (BN / 2) : nt * BN);
+      return make_rsrc(B + b_row0 * K,
+                       (uint32_t)min((size_t)0x7fffffff, ((size_t)(slot + 1) * NW - b_row0) * K * 2));
+    };
+    auto a_of = [&](int row0, int rows) {
+      return GATHER ? make_rsrc(A, (uint32_t)A_rows * K * 2)
+                    : make_rsrc(A + (size_t)row0 * K, (uint32_t)rows * K * 2);
+    };
+    // Byte offsets of this lane's A chunks for a tile. GATHER: the RPI rows of
+    // each load instruction come in by scalar loads of perm (clamped to the
+    // tile's last row), pair index / kq by multiply-high with the host's
+    // magic number, and each lane picks its row; rows past the end read as
+    // zeros.
+    auto a_offsets = [&](int row0, int rows, int* a_off) {
 #pragma unroll
-    for (int i = 0; i < AI; ++i) {
-      const int r = wave * RW + i * RPI + lane / CH;
-      const int cc = ((lane % CH) ^ swz<CH>(r)) * 8;
-      if (GATHER) {
-        int t = pv[i * RPI];
+      for (int i = 0; i < AI; ++i) {
+        const int r = wave * RW + i * RPI + lane / CH;
+        const int cc = ((lane % CH) ^ swz<CH>(r)) * 8;
+        if (GATHER) {
+          int t = 0;
 #pragma unroll
-        for (int j = 1; j < RPI; ++j) t = (lane / CH == j) ? pv[i * RPI + j] : t;
-        a_off[i] = (r < rows) ? (t * K + cc) * 2 : (int)0x80000000u;
-      } else {
-        a_off[i] = (r * K + cc) * 2;
-      }
-    }
-  };
-
-  int b_off[BI];
-#pragma unroll
-  for (int i = 0; i < BI; ++i) {
-    const int r = wave * (BN / NWAVE) + i * RPI + lane / CH;
-    const int wr = (SWIGLU && r >= BN / 2) ? I - BN / 2 + r : r;
-    b_off[i] = (wr * K + ((lane % CH) ^ swz<CH>(r)) * 8) * 2;
-  }
-  lds_u16* const smem3 = (lds_u16*)smem;
-  const int a_lds = wave * RW * BK;
-  const int b_lds = 2 * A_ST + wave * (BN / NWAVE) * BK;
-#define TG_ISSUE_A(rs, offs, k0, buf)                                                   \
-  do {                                                                                  \
-    _Pragma("unroll") for (int i = 0; i < AI; ++i)                                      \
-        load_lds16(rs, smem3 + (buf) * A_ST + a_lds + i * RPI * BK, offs[i], (k0) * 2); \
-  } while (0)
-#define TG_ISSUE_B(rs, k0, buf)                                                          \
-  do {                                                                                   \
-    _Pragma("unroll") for (int i = 0; i < BI; ++i)                                       \
-        load_lds16(rs, smem3 + (buf) * B_ST + b_lds + i * RPI * BK, b_off[i], (k0) * 2); \
-  } while (0)
-  const int khalf = lane >> 5;
-  const int xrow = wm * (BM / WM) + (lane & 31);
-  const int wrow = (SWIGLU ? wn * (BN / 2 / WN) : wn * (BN / WN)) + (lane & 31);
-  int xoff[BK / 16], woff[BK / 16];
-#pragma unroll
-  for (int kk = 0; kk < BK / 16; ++kk) {
-    xoff[kk] = xrow * BK + (((2 * kk + khalf) ^ swz<CH>(xrow)) << 3);
-    woff[kk] = 2 * A_ST + wrow * BK + (((2 * kk + khalf) ^ swz<CH>(wrow)) << 3);
-  }
-  auto wblk = [](int nb) constexpr {
-    return SWIGLU ? ((nb < NB / 2) ? nb * 32 : BN / 2 + (nb - NB / 2) * 32) : nb * 32;
-  };
-  const int nk = K / BK;  // at least 3 (checked by the launcher)
-  constexpr int KK = BK / 16;
-  static_assert(KK % 2 == 0, "fragment double buffering alternates within a stage");
-  bf16x8 xf[2][MB], wf[2][NB];
-  f32x16 acc[NB][MB];
-#define TG_FRAGS(abuf, bbuf, kk, dst)                                                       \
-  do {                                                                                      \
-    _Pragma("unroll") for (int mb = 0; mb < MB; ++mb) xf[dst][mb] =                         \
-        *reinterpret_cast<const bf16x8*>(smem + (abuf) * A_ST + xoff[kk] + mb * 32 * BK);   \
-    _Pragma("unroll") for (int nb = 0; nb < NB; ++nb) wf[dst][nb] =                         \
-        *reinterpret_cast<const bf16x8*>(smem + (bbuf) * B_ST + woff[kk] + wblk(nb) * BK);  \
-  } while (0)
-#define TG_MFMAS(src)                                                                       \
-  do {                                                                                      \
-    _Pragma("unroll") for (int nb = 0; nb < NB; ++nb)                                       \
-        _Pragma("unroll") for (int mb = 0; mb < MB; ++mb) acc[nb][mb] =                     \
-            __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[src][nb], xf[src][mb], acc[nb][mb],  \
-                                                    0, 0, 0);                               \
-  } while (0)
-  // Refill of the buffers of the stage just consumed: A of stage kt+2 and B
-  // of stage kt+3 of this tile, else of the next tile, else (no next tile)
-  // the last stage again into buffers nobody reads any more.
-#define TG_REFILL(kt)                                                                       \
-  do {                                                                                      \
-    const bool ca = (kt) + 2 < nk, cb = (kt) + 3 < nk;                                      \
-    const int ka = ca ? (kt) + 2 : (has_n ? (kt) + 2 - nk : nk - 1);                        \
-    const int kb = cb ? (kt) + 3 : (has_n ? (kt) + 3 - nk : nk - 1);                        \
-    if (ca || !has_n) TG_ISSUE_A(a_cur, a_off, ka * BK, ab);                                \
-    else TG_ISSUE_A(a_n, a_off_n, ka * BK, ab);                                             \
-    TG_ISSUE_B((cb || !has_n) ? b_cur : b_n, kb * BK, bb);                                  \
-  } while (0)
-
-  int slot, row0, rows, nt;
-  seek(L, slot, row0, rows, nt);
-  __amdgpu_buffer_rsrc_t a_cur = a_of(row0, rows), b_cur = b_of(slot, nt);
-  int a_off[AI], a_off_n[AI];
-  a_offsets(row0, rows, a_off);
-  int Ln = L + per_xcd_blocks;
-  bool has_n = Ln < hi;
-  int slot_n = slot, row0_n = row0, rows_n = rows, nt_n = nt;
-  if (has_n) seek(Ln, slot_n, row0_n, rows_n, nt_n);
-  __amdgpu_buffer_rsrc_t a_n = a_of(row0_n, rows_n), b_n = b_of(slot_n, nt_n);
-  a_offsets(row0_n, rows_n, a_off_n);
-
-  TG_ISSUE_A(a_cur, a_off, 0, 0);
-  TG_ISSUE_B(b_cur, 0, 0);
-  TG_ISSUE_B(b_cur, BK, 1);
-  TG_ISSUE_A(a_cur, a_off, BK, 1);
-  TG_ISSUE_B(b_cur, 2 * BK, 2);
-  TG_WAIT_VM(2 * BI + AI);
-  block_barrier();
-  TG_FRAGS(0, 0, 0, 0);
-
-  int ab = 0, bb = 0;  // buffers of the current stage (stages count on across tiles)
-  for (;;) {
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-      for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) acc[nb][mb][r] = 0.0f;
-    const bool active = wm * (BM / WM) < rows;
-    if (active) {
-      for (int kt = 0; kt < nk; ++kt) {
-#pragma unroll
-        for (int kk = 0; kk < KK - 1; ++kk) {
-          TG_FRAGS(ab, bb, kk + 1, (kk + 1) & 1);
-          TG_MFMAS(kk & 1);
+          for (int j = 0; j < RPI; ++j) {
+            const uint32_t pj = (uint32_t)perm[row0 + min(wave * RW + i * RPI + j, rows - 1)];
+            const int tj = (int)(kq_shift ? __umulhi(pj, kq_magic) >> (kq_shift - 1) : pj);
+            t = (lane / CH == j) ? tj : t;
+          }
+          a_off[i] = (r < rows) ? (t * K + cc) * 2 : (int)0x80000000u;
+        } else {
+          a_off[i] = (r * K + cc) * 2;
         }
-        TG_WAIT_VM(BI);
-        __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)
-        block_barrier();
-        TG_REFILL(kt);
-        ab ^= 1;
-        bb = (bb == 2) ? 0 : bb + 1;
-        TG_FRAGS(ab, bb, 0, 0);
-        TG_MFMAS((KK - 1) & 1);
       }
-    } else {
-      for (int kt = 0; kt < nk; ++kt) {
-        TG_WAIT_VM(BI);
-        block_barrier();
-        TG_REFILL(kt);
-        ab ^= 1;
-        bb = (bb == 2) ? 0 : bb + 1;
-      }
-      TG_FRAGS(ab, bb, 0, 0);
+    };
+
+    int b_off[BI];
+#pragma unroll
+    for (int i = 0; i < BI; ++i) {
+      const int r = wave * (BN / NWAVE) + i * RPI + lane / CH;
+      const int wr = (SWIGLU && r >= BN / 2) ? I - BN / 2 + r : r;
+      b_off[i] = (wr * K + ((lane % CH) ^ swz<CH>(r)) * 8) * 2;
     }
-    // acc[nb][mb] register r of lane l: row mb*32 + l%32, column
-    // nb*32 + 8*(r/4) + 4*(l/32) + r%4 of the wave's sub-tile.
-    if (active) {
-      const int colbase = SWIGLU ? nt * (BN / 2) + wn * WOUT : nt * BN + wn * WOUT;
+    lds_u16* const smem3 = (lds_u16*)smem;
+    const int a_lds = wave * RW * BK;
+    const int b_lds = 2 * A_ST + wave * (BN / NWAVE) * BK;
+    const int khalf = lane >> 5;
+    const int xrow = wm * (BM / WM) + (lane & 31);
+    const int wrow = (SWIGLU ? wn * (BN / 2 / WN) : wn * (BN / WN)) + (lane & 31);
+    int xoff[KK], woff[KK];
 #pragma unroll
-      for (int mb = 0; mb < MB; ++mb) {
-        const int r = wm * (BM / WM) + mb * 32 + (lane & 31);
-        uint16_t* crow = C + (size_t)(row0 + r) * ldc + colbase + 4 * (lane >> 5);
+    for (int kk = 0; kk < KK; ++kk) {
+      xoff[kk] = xrow * BK + (((2 * kk + khalf) ^ swz<CH>(xrow)) << 3);
+      woff[kk] = 2 * A_ST + wrow * BK + (((2 * kk + khalf) ^ swz<CH>(wrow)) << 3);
+    }
+    auto wblk = [](int nb) constexpr {
+      return SWIGLU ? ((nb < NB / 2) ? nb * 32 : BN / 2 + (nb - NB / 2) * 32) : nb * 32;
+    };
+    const int nk = K / BK;  // at least 3 (checked by the launcher)
+    bf16x8 xf[2][MB], wf[2][NB];
+    f32x16 acc[NB][MB];
+
+#define TG_ISSUE_A(rs, offs, k0, buf, i0, i1)                                              \
+  do {                                                                                     \
+    _Pragma("unroll") for (int i = (i0); i < (i1); ++i)                                    \
+        load_lds16(rs, smem3 + (buf) * A_ST + a_lds + i * RPI * BK, offs[i], (k0) * 2);    \
+  } while (0)
+#define TG_ISSUE_B(rs, k0, buf, i0, i1)                                                    \
+  do {                                                                                     \
+    _Pragma("unroll") for (int i = (i0); i < (i1); ++i)                                    \
+        load_lds16(rs, smem3 + (buf) * B_ST + b_lds + i * RPI * BK, b_off[i], (k0) * 2);   \
+  } while (0)
+#define TG_FRAGS(abuf, bbuf, kk, dst)                                                      \
+  do {                                                                                     \
+    _Pragma("unroll") for (int mb = 0; mb < MB; ++mb) xf[dst][mb] =                        \
+        *reinterpret_cast<const bf16x8*>(smem + (abuf) * A_ST + xoff[kk] + mb * 32 * BK);  \
+    _Pragma("unroll") for (int nb = 0; nb < NB; ++nb) wf[dst][nb] =                        \
+        *reinterpret_cast<const bf16x8*>(smem + (bbuf) * B_ST + woff[kk] + wblk(nb) * BK); \
+  } while (0)
+#define TG_MFMAS(src, lo_, hi_)                                                            \
+  do {                                                                                     \
+    _Pragma("unroll") for (int q = (lo_); q < (hi_); ++q) acc[q / MB][q % MB] =            \
+        __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[src][q / MB], xf[src][q % MB],          \
+                                                acc[q / MB][q % MB], 0, 0, 0);             \
+  } while (0)
+#define TG_SG(mask, n) __builtin_amdgcn_sched_group_barrier(mask, n, 0)
+    // Scheduling groups: 0x008 MFMA, 0x010 VMEM, 0x100 DS read.
+  // Each sub-step spreads the 8 fragment reads of the next sub-step over its
+  // first 8 MFMAs, then issues 4 of the stage's 16 DMA loads among the other
+  // 8, so that neither the LDS queue nor the load path (about 16 cycles per
+  // 1 KB load) backs up far enough to stall the wave's instruction stream.
+  // The fragment reads come before the loads: the compiler keeps every LDS
+  // read ahead of the DMA writes that follow it in program order (it cannot
+  // tell that they touch other buffers).
+#define TG_PATTERN_LOADS                                                                   \
+  do {                                                                                     \
+    _Pragma("unroll") for (int i = 0; i < 8; ++i) {                                        \
+      TG_SG(0x100, 1);                                                                     \
+      TG_SG(0x008, 1);                                                                     \
+    }                                                                                      \
+    _Pragma("unroll") for (int i = 0; i < 4; ++i) {                                        \
+      TG_SG(0x010, 1);                                                                     \
+      TG_SG(0x008, 2);                                                                     \
+    }                                                                                      \
+  } while (0)
+#define TG_PATTERN_LOADS_HALF                                                              \
+  do {                                                                                     \
+    _Pragma("unroll") for (int i = 0; i < 4; ++i) {                                        \
+      TG_SG(0x008, 1);                                                                     \
+      TG_SG(0x010, 1);                                                                     \
+      TG_SG(0x008, 1);                                                                     \
+    }                                                                                      \
+  } while (0)
+#define TG_PATTERN_FRAGS(nm)                                                               \
+  do {                                                                                     \
+    _Pragma("unroll") for (int i = 0; i < 8; ++i) {                                        \
+      TG_SG(0x100, 1);                                                                     \
+      TG_SG(0x008, (nm) / 8);                                                              \
+    }                                                                                      \
+  } while (0)
+
+    int slot, row0, rows, nt;
+    seek(L, slot, row0, rows, nt);
+    __amdgpu_buffer_rsrc_t a_cur = a_of(row0, rows), b_cur = b_of(slot, nt);
+    int a_off[AI], a_off_n[AI];
+    a_offsets(row0, rows, a_off);
+    int Ln = L + per_xcd_blocks;
+    bool has_n = Ln < hi;
+    int slot_n = slot, row0_n = row0, rows_n = rows, nt_n = nt;
+    if (has_n) seek(Ln, slot_n, row0_n, rows_n, nt_n);
+    __amdgpu_buffer_rsrc_t a_n = a_of(row0_n, rows_n), b_n = b_of(slot_n, nt_n);
+    a_offsets(row0_n, rows_n, a_off_n);
+
+    // Prologue: A and B of stage 0, B of stage 1; stage 0 visible; its first
+    // fragments read.
+    TG_ISSUE_A(a_cur, a_off, 0, 0, 0, AI);
+    TG_ISSUE_B(b_cur, 0, 0, 0, BI);
+    TG_ISSUE_B(b_cur, BK, 1, 0, BI);
+    TG_WAIT_VM(BI);
+    block_barrier();
+    TG_FRAGS(0, 0, 0, 0);
+
+    int ab = 0, bb = 0;  // buffers of the current stage
+    for (;;) {
 #pragma unroll
-        for (int nb = 0; nb < (SWIGLU ? NB / 2 : NB); ++nb) {
+      for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            float v[4];
+        for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              const int rr = 4 * q + e;
-              if (SWIGLU) {
-                const float g = acc[nb][mb][rr];
-                const float u = acc[nb + NB / 2][mb][rr];
-                v[e] = g / (1.0f + __expf(-g)) * u;
-              } else {
-                v[e] = acc[nb][mb][rr];
+          for (int r = 0; r < 16; ++r) acc[nb][mb][r] = 0.0f;
+      const bool active = wm * (BM / WM) < rows;
+      // A of stage kt+1 and B of stage kt+2 go into the buffers released at
+      // the previous barrier: this tile's, else the next tile's, else (no
+      // next tile) this tile's last stage again.
+#define TG_TARGETS(kt)                                                                     \
+  const bool ca = (kt) + 1 < nk, cb = (kt) + 2 < nk;                                       \
+  const int ka = ca ? (kt) + 1 : (has_n ? (kt) + 1 - nk : nk - 1);                         \
+  const int kb = cb ? (kt) + 2 : (has_n ? (kt) + 2 - nk : nk - 1);                         \
+  const bool a_here = ca || !has_n;                                                        \
+  const __amdgpu_buffer_rsrc_t ra = a_here ? a_cur : a_n;                                  \
+  const __amdgpu_buffer_rsrc_t rb = (cb || !has_n) ? b_cur : b_n;                          \
+  int offa[AI];                                                                            \
+  _Pragma("unroll") for (int i = 0; i < AI; ++i) offa[i] = a_here ? a_off[i] : a_off_n[i]; \
+  const int abn = ab ^ 1, bbn = (bb == 0) ? 2 : bb - 1
+      if (active) {
+        for (int kt = 0; kt < nk; ++kt) {
+          TG_TARGETS(kt);
+          TG_FRAGS(ab, bb, 1, 1);
+          TG_ISSUE_A(ra, offa, ka * BK, abn, 0, AI / 2);
+          TG_MFMAS(0, 0, 16);
+          TG_PATTERN_LOADS;
+          __builtin_amdgcn_sched_barrier(0);
+          TG_FRAGS(ab, bb, 2, 0);
+          TG_ISSUE_A(ra, offa, ka * BK, abn, AI / 2, AI);
+          TG_MFMAS(1, 0, 16);
+          TG_PATTERN_LOADS;
+          __builtin_amdgcn_sched_barrier(0);
+          TG_FRAGS(ab, bb, 3, 1);
+          TG_ISSUE_B(rb, kb * BK, bbn, 0, BI / 2);
+          TG_MFMAS(0, 0, 16);
+          TG_PATTERN_LOADS;
+          __builtin_amdgcn_sched_barrier(0);
+          __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this stage's buffers are read
+          TG_ISSUE_B(rb, kb * BK, bbn, BI / 2, BI);
+          TG_MFMAS(1, 0, 8);
+          TG_PATTERN_LOADS_HALF;
+          __builtin_amdgcn_sched_barrier(0);
+          TG_WAIT_VM(BI);
+          block_barrier();
+          ab ^= 1;
+          bb = (bb == 2) ? 0 : bb + 1;
+          TG_FRAGS(ab, bb, 0, 0);
+          TG_MFMAS(1, 8, 16);
+          TG_PATTERN_FRAGS(8);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      } else {
+        __builtin_amdgcn_s_waitcnt(0xc07f);  // fragment reads of the previous tile
+        for (int kt = 0; kt < nk; ++kt) {
+          TG_TARGETS(kt);
+          TG_ISSUE_A(ra, offa, ka * BK, abn, 0, AI);
+          TG_ISSUE_B(rb, kb * BK, bbn, 0, BI);
+          TG_WAIT_VM(BI);
+          block_barrier();
+          ab ^= 1;
+          bb = (bb == 2) ? 0 : bb + 1;
+        }
+        TG_FRAGS(ab, bb, 0, 0);
+      }
+#undef TG_TARGETS
+      // acc[nb][mb] register r of lane l: row mb*32 + l%32, column
+      // nb*32 + 8*(r/4) + 4*(l/32) + r%4 of the wave's sub-tile.
+      if (active) {
+        const int colbase = SWIGLU ? nt * (BN / 2) + wn * WOUT : nt * BN + wn * WOUT;
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) {
+          const int r = wm * (BM / WM) + mb * 32 + (lane & 31);
+          uint16_t* crow = C + (size_t)(row0 + r) * ldc + colbase + 4 * (lane >> 5);
+#pragma unroll
+          for (int nb = 0; nb < (SWIGLU ? NB / 2 : NB); ++nb) {
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              float v[4];
+#pragma unroll
+              for (int e = 0; e < 4; ++e) {
+                const int rr = 4 * q + e;
+                if (SWIGLU) {
+                  const float g = acc[nb][mb][rr];
+                  const float u = acc[nb + NB / 2][mb][rr];
+                  v[e] = swiglu(g, u);
+                } else {
+                  v[e] = acc[nb][mb][rr];
+                }
               }
+              uint2 pk;
+              pk.x = pack_bf16x2(v[0], v[1]);
+              pk.y = pack_bf16x2(v[2], v[3]);
+              if (r < rows) *reinterpret_cast<uint2*>(crow + nb * 32 + 8 * q) = pk;
             }
-            uint2 pk;
-            pk.x = pack_bf16x2(v[0], v[1]);
-            pk.y = pack_bf16x2(v[2], v[3]);
-            if (r < rows) *reinterpret_cast<uint2*>(crow + nb * 32 + 8 * q) = pk;
           }
         }
       }
-    }
-    if (!has_n) break;
-    row0 = row0_n;
-    rows = rows_n;
-    nt = nt_n;
-    a_cur = a_n;
-    b_cur = b_n;
+      if (!has_n) break;
+      row0 = row0_n;
+      rows = rows_n;
+      nt = nt_n;
+      a_cur = a_n;
+      b_cur = b_n;
 #pragma unroll
-    for (int i = 0; i < AI; ++i) a_off[i] = a_off_n[i];
-    Ln += per_xcd_blocks;
-    has_n = Ln < hi;
-    if (has_n) {
-      seek(Ln, slot_n, row0_n, rows_n, nt_n);
-      a_n = a_of(row0_n, rows_n);
-      b_n = b_of(slot_n, nt_n);
-      a_offsets(row0_n, rows_n, a_off_n);
+      for (int i = 0; i < AI; ++i) a_off[i] = a_off_n[i];
+      Ln += per_xcd_blocks;
+      has_n = Ln < hi;
+      if (has_n) {
+        seek(Ln, slot_n, row0_n, rows_n, nt_n);
+        a_n = a_of(row0_n, rows_n);
+        b_n = b_of(slot_n, nt_n);
+        a_offsets(row0_n, rows_n, a_off_n);
+      }
     }
-  }
-  TG_WAIT_VM(0);  // no LDS write may land after the walk
-#undef TG_REFILL
+    TG_WAIT_VM(0);  // no LDS write may land after the walk
+#undef TG_PATTERN_FRAGS
+#undef TG_PATTERN_LOADS_HALF
+#undef TG_PATTERN_LOADS
+#undef TG_SG
 #undef TG_FRAGS
 #undef TG_MFMAS
 #undef TG_ISSUE_A
@@ -694,9 +754,6 @@ __global__ __launch_bounds__(64 * WM * WN) void grouped_gemm_persistent_kernel(
   }
   if constexpr (TAIL) {
     if (!tail) return;
-    // Quarter q of the tail: tile n_head + q / 4, row half (q % 4) / 2,
-    // column half q % 2; the XCD's share of the quarters, one at a time
-    // (each with its own pipeline and LDS epilogue).
     __syncthreads();
     const int nq = 4 * rem;
     const int qper = (nq + kXcds - 1) / kXcds;
@@ -711,8 +768,8 @@ __global__ __launch_bounds__(64 * WM * WN) void grouped_gemm_persistent_kernel(
       if (rows > 0) {
         t.row0 += m * (BM / 2);
         t.rows = rows;
-        gemm_tile<BM / 2, BN / 2, BK, WMq, WNq, SWIGLU, GATHER>(smem, t, A, B, K, NW, I, C, ldc,
-                                                                perm, 1, A_rows);
+        gemm_tile<BM / 2, BN / 2, BK, 2, 2, SWIGLU, GATHER>(smem, t, A, B, K, NW, I, C, ldc, perm, 1,
+                                                         A_rows);
         __syncthreads();
       }
     }
@@ -755,32 +812,21 @@ hipError_t launch_grouped(const uint16_t* A, const int32_t* offsets, int S, int 
   return hipGetLastError();
 }
 
-// Persistent launch: one block per CU (a multiple of 8), for K of at least 3
-// stages.
-template <int BM, int BN, int BK, int WM, int WN, bool SWIGLU, bool GATHER, bool TAIL = false,
-          int WMq = WM, int WNq = WN>
-hipError_t launch_persistent(const uint16_t* A, const int32_t* offsets, int S, const uint16_t* B,
-                             int K, int NW, int I, uint16_t* C, int ldc, int NT,
-                             hipStream_t stream, const int32_t* perm, int kq, int A_rows) {
-  // n / kq = mulhi(n, m) >> (l - 1) for every n < 2^31, with l = ceil(log2 kq)
-  // and m = ceil(2^(31 + l) / kq) < 2^32 (division by an invariant integer).
+// Launch of the 4-wave persistent kernel: one block per CU (a multiple of
+// 8); K of at least 2 stages (d is a multiple of 256, I of 128).
+template <bool SWIGLU, bool GATHER, bool TAIL>
+hipError_t launch_persistent4(const uint16_t* A, const int32_t* offsets, int S, const uint16_t* B,
+                              int K, int NW, int I, uint16_t* C, int ldc, int NT,
+                              hipStream_t stream, const int32_t* perm, int kq, int A_rows) {
   int l = 0;
   while ((1 << l) < kq) ++l;
   const uint32_t m = (uint32_t)((((uint64_t)1 << (31 + l)) + (uint64_t)kq - 1) / (uint64_t)kq);
   const int grid = cu_count() / kXcds * kXcds;
-  hipLaunchKernelGGL(
-      (grouped_gemm_persistent_kernel<BM, BN, BK, WM, WN, SWIGLU, GATHER, TAIL, WMq, WNq>),
-      dim3(grid), dim3(64 * WM * WN), 0, stream, A, offsets, S, B, K, NW, I, C, ldc, NT, perm, m,
-      l, A_rows);
+  hipLaunchKernelGGL((grouped_gemm_persistent4_kernel<SWIGLU, GATHER, TAIL>), dim3(grid), dim3(256),
+                     0, stream, A, offsets, S, B, K, NW, I, C, ldc, NT, perm, m, l, A_rows);
   return hipGetLastError();
 }
 
-// Small-batch tile shape (BM, BN, BK, WM, WN); the full-size shape is
-// 256 x 256 x 64 with 4 x 4 waves (persistent kernel).
-// Large: 256 x 256, 16 waves; the down projection runs its tail as 128 x 128
-// quarter tiles with the same 16 waves (the gate/up projection's quarter
-// tiles would need an even number of 32-column blocks per wave, hence at most
-// 8 waves, so it runs its tail at full size). Small: 32 x 256, 4 waves.
 #define TG_SMALL 32, 256, 64, 1, 4
 constexpr int kBN = 256;
 constexpr int kSmallRowsPerSlot = 32;
@@ -795,9 +841,8 @@ hipError_t launch_ffn_gateup(const uint16_t* x_perm, const int32_t* offsets, int
   if (small_batch(S, max_rows))
     return launch_grouped<TG_SMALL, true, false>(x_perm, offsets, S, max_rows, w13, d,
                                                         2 * I, I, h, I, (2 * I) / kBN, stream);
-  return launch_persistent<256, 256, 64, 4, 4, true, false>(x_perm, offsets, S, w13, d, 2 * I, I,
-                                                            h, I, (2 * I) / kBN, stream, nullptr, 1,
-                                                            0);
+  return launch_persistent4<true, false, false>(x_perm, offsets, S, w13, d, 2 * I, I, h, I,
+                                                (2 * I) / kBN, stream, nullptr, 1, 0);
 }
 
 hipError_t launch_ffn_gateup_gather(const uint16_t* x, int T, const int32_t* perm, int k,
@@ -808,8 +853,8 @@ hipError_t launch_ffn_gateup_gather(const uint16_t* x, int T, const int32_t* per
   if (small_batch(S, max_rows))
     return launch_grouped<TG_SMALL, true, true>(x, offsets, S, max_rows, w13, d, 2 * I, I,
                                                        h, I, (2 * I) / kBN, stream, perm, k, T);
-  return launch_persistent<256, 256, 64, 4, 4, true, true>(x, offsets, S, w13, d, 2 * I, I, h, I,
-                                                           (2 * I) / kBN, stream, perm, k, T);
+  return launch_persistent4<true, true, false>(x, offsets, S, w13, d, 2 * I, I, h, I,
+                                               (2 * I) / kBN, stream, perm, k, T);
 }
 
 hipError_t launch_ffn_down(const uint16_t* h, const int32_t* offsets, int S, int max_rows,
@@ -818,8 +863,8 @@ hipError_t launch_ffn_down(const uint16_t* h, const int32_t* offsets, int S, int
   if (small_batch(S, max_rows))
     return launch_grouped<TG_SMALL, false, false>(h, offsets, S, max_rows, w2, I, d, 0, y,
                                                          d, d / kBN, stream);
-  return launch_persistent<256, 256, 64, 4, 4, false, false, true, 4, 4>(
-      h, offsets, S, w2, I, d, 0, y, d, d / kBN, stream, nullptr, 1, 0);
+  return launch_persistent4<false, false, true>(h, offsets, S, w2, I, d, 0, y, d, d / kBN, stream,
+                                                nullptr, 1, 0);
 }
 
 hipError_t launch_expert_ffn(const uint16_t* x_perm, const int32_t* offsets, int S, int max_rows,
