@@ -54,6 +54,8 @@
 // in increasing order, independent of the row's position, its tile or the
 // other rows of its group; a row therefore gives identical bits in any slot
 // holding the same weights (shadow failover, §5.3).
+#include <type_traits>
+
 #include "tg_device.h"
 #include "tg_launch.h"
 
@@ -412,39 +414,45 @@ __device__ __forceinline__ void gemm_tile(uint16_t* smem, const TileInfo& tile,
   }
 }
 
-// Persistent kernel with one wave per SIMD: 4 waves (2 x 2), each computing
-// 128 x 128 of the 256 x 256 tile, so each fragment read from LDS feeds four
-// MFMAs instead of two. That halves the LDS read traffic of the 16-wave
-// shape, and under the power limit the clock stays higher. With a single
-// wave per SIMD no other wave covers a gap in the instruction stream, so the
-// order within a stage of four k16 sub-steps is fixed explicitly:
-//   sub-steps 0-2: 16 MFMAs with the next sub-step's fragment reads and a
+// Persistent kernel with one wave per SIMD: 4 waves, 256 x 256 tiles. A
+// tile with more than 128 rows runs in full mode: waves (wm, wn) of a 2 x 2
+// grid each compute 128 x 128 (4 x 4 blocks of 32 x 32), so each fragment
+// read from LDS feeds four MFMAs instead of two; that halves the LDS read
+// traffic of a 16-wave shape, and under the power limit the clock stays
+// higher. The last row block of a slot is usually partial: with at most 128
+// rows the tile runs in half mode (every wave rows 0-127 and a quarter of the
+// columns, 4 x 2 blocks), with at most 64 rows in quarter mode (rows 0-63,
+// 2 x 2 blocks), so its cost follows its rows instead of a full tile's.
+// The 32 x 32 blocks stay aligned in every mode, so each output element gets
+// the same MFMA sequence, hence the same bits.
+//
+// With a single wave per SIMD no other wave covers a gap in the instruction
+// stream, so the order within a stage of four k16 sub-steps is fixed
+// explicitly:
+//   sub-steps 0-2: the MFMAs with the next sub-step's fragment reads and a
 //               quarter of the stage's DMA loads among them (A in sub-steps
 //               0 and 1, B in sub-step 2);
-//   sub-step 3: 8 MFMAs with the last quarter of the loads, then the wait
-//               and the block barrier while they run, then the next stage's
-//               first fragments interleaved with the other 8 MFMAs.
+//   sub-step 3: half of its MFMAs with the last quarter of the loads, then
+//               the wait and the block barrier while they run, then the next
+//               stage's first fragments interleaved with the other half.
 // During stage g (counted on across tiles) A of stage g+1 and B of stage g+2
 // are loaded into the buffers that stage g-1 released at the previous
 // barrier; at the end of stage g only B of stage g+2 may still be in flight.
 // Loads past the last stage of the walk re-load that stage into released
-// buffers, so every wait counts the same number of loads. Same MFMA sequence
-// per output element as the other kernels, hence the same bits.
+// buffers, so every wait counts the same number of loads.
 template <bool SWIGLU, bool GATHER, bool TAIL>
 __global__ __launch_bounds__(256) void grouped_gemm_persistent4_kernel(
     const uint16_t* __restrict__ A, const int32_t* __restrict__ offsets, int S,
     const uint16_t* __restrict__ B, int K, int NW, int I, uint16_t* __restrict__ C, int ldc,
     int NT, const int32_t* __restrict__ perm, uint32_t kq_magic, int kq_shift, int A_rows) {
-  constexpr int BM = 256, BN = 256, BK = 64, WM = 2, WN = 2, NWAVE = WM * WN;
-  constexpr int MB = BM / WM / 32, NB = BN / WN / 32;  // 4 x 4 blocks of 32 x 32 per wave
+  constexpr int BM = 256, BN = 256, BK = 64, NWAVE = 4;
   constexpr int CH = BK / 8;                            // 16-byte chunks per staged row
   constexpr int RPI = 64 / CH;                          // staged rows per load instruction
   constexpr int RW = BM / NWAVE;                        // staged A rows per wave
   constexpr int AI = RW / RPI, BI = BN / NWAVE / RPI;   // load instructions per stage
   constexpr int A_ST = BM * BK, B_ST = BN * BK;
-  constexpr int WOUT = SWIGLU ? BN / 2 / WN : BN / WN;
   constexpr int KK = BK / 16;
-  static_assert(KK == 4 && AI == 8 && BI == 8 && MB * NB == 16, "schedule assumes this shape");
+  static_assert(KK == 4 && AI == 8 && BI == 8, "schedule assumes this shape");
   static_assert(!(TAIL && GATHER), "quarter tiles read pre-permuted rows");
   __shared__ __attribute__((aligned(16))) uint16_t smem[2 * A_ST + 3 * B_ST];
 
@@ -461,7 +469,7 @@ __global__ __launch_bounds__(256) void grouped_gemm_persistent4_kernel(
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int wm = wave / WN, wn = wave % WN;
+    const int wm = wave >> 1, wn = wave & 1;
 
     int s_cur = 0, before = 0, pos = 0, c_nt = 0, c_m = 0;
     int o_cur = offsets[0];
@@ -530,20 +538,7 @@ __global__ __launch_bounds__(256) void grouped_gemm_persistent4_kernel(
     const int a_lds = wave * RW * BK;
     const int b_lds = 2 * A_ST + wave * (BN / NWAVE) * BK;
     const int khalf = lane >> 5;
-    const int xrow = wm * (BM / WM) + (lane & 31);
-    const int wrow = (SWIGLU ? wn * (BN / 2 / WN) : wn * (BN / WN)) + (lane & 31);
-    int xoff[KK], woff[KK];
-#pragma unroll
-    for (int kk = 0; kk < KK; ++kk) {
-      xoff[kk] = xrow * BK + (((2 * kk + khalf) ^ swz<CH>(xrow)) << 3);
-      woff[kk] = 2 * A_ST + wrow * BK + (((2 * kk + khalf) ^ swz<CH>(wrow)) << 3);
-    }
-    auto wblk = [](int nb) constexpr {
-      return SWIGLU ? ((nb < NB / 2) ? nb * 32 : BN / 2 + (nb - NB / 2) * 32) : nb * 32;
-    };
-    const int nk = K / BK;  // at least 3 (checked by the launcher)
-    bf16x8 xf[2][MB], wf[2][NB];
-    f32x16 acc[NB][MB];
+    const int nk = K / BK;  // at least 2 (checked by the launcher)
 
 #define TG_ISSUE_A(rs, offs, k0, buf, i0, i1)                                              \
   do {                                                                                     \
@@ -557,52 +552,75 @@ __global__ __launch_bounds__(256) void grouped_gemm_persistent4_kernel(
   } while (0)
 #define TG_FRAGS(abuf, bbuf, kk, dst)                                                      \
   do {                                                                                     \
-    _Pragma("unroll") for (int mb = 0; mb < MB; ++mb) xf[dst][mb] =                        \
+    _Pragma("unroll") for (int mb = 0; mb < MBm; ++mb) xf[dst][mb] =                       \
         *reinterpret_cast<const bf16x8*>(smem + (abuf) * A_ST + xoff[kk] + mb * 32 * BK);  \
-    _Pragma("unroll") for (int nb = 0; nb < NB; ++nb) wf[dst][nb] =                        \
+    _Pragma("unroll") for (int nb = 0; nb < NBm; ++nb) wf[dst][nb] =                       \
         *reinterpret_cast<const bf16x8*>(smem + (bbuf) * B_ST + woff[kk] + wblk(nb) * BK); \
   } while (0)
 #define TG_MFMAS(src, lo_, hi_)                                                            \
   do {                                                                                     \
-    _Pragma("unroll") for (int q = (lo_); q < (hi_); ++q) acc[q / MB][q % MB] =            \
-        __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[src][q / MB], xf[src][q % MB],          \
-                                                acc[q / MB][q % MB], 0, 0, 0);             \
+    _Pragma("unroll") for (int q = (lo_); q < (hi_); ++q) acc[q / MBm][q % MBm] =          \
+        __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[src][q / MBm], xf[src][q % MBm],        \
+                                                acc[q / MBm][q % MBm], 0, 0, 0);           \
   } while (0)
 #define TG_SG(mask, n) __builtin_amdgcn_sched_group_barrier(mask, n, 0)
-    // Scheduling groups: 0x008 MFMA, 0x010 VMEM, 0x100 DS read.
-  // Each sub-step spreads the 8 fragment reads of the next sub-step over its
-  // first 8 MFMAs, then issues 4 of the stage's 16 DMA loads among the other
-  // 8, so that neither the LDS queue nor the load path (about 16 cycles per
-  // 1 KB load) backs up far enough to stall the wave's instruction stream.
-  // The fragment reads come before the loads: the compiler keeps every LDS
-  // read ahead of the DMA writes that follow it in program order (it cannot
-  // tell that they touch other buffers).
+#define TG_DM TG_SG(0x100, 1); TG_SG(0x008, 1)
+    // Scheduling groups: 0x008 MFMA, 0x010 VMEM, 0x100 DS read. In sub-steps
+    // 0-2 the fragment reads of the next sub-step are spread over the first
+    // MFMAs and the sub-step's 4 DMA loads over the rest, so that neither the
+    // LDS queue nor the load path (about 16 cycles per 1 KB load) backs up
+    // far enough to stall the wave's instruction stream. The fragment reads
+    // come before the loads: the compiler keeps every LDS read ahead of the
+    // DMA writes that follow it in program order (it cannot tell that they
+    // touch other buffers).
 #define TG_PATTERN_LOADS                                                                   \
   do {                                                                                     \
-    _Pragma("unroll") for (int i = 0; i < 8; ++i) {                                        \
-      TG_SG(0x100, 1);                                                                     \
-      TG_SG(0x008, 1);                                                                     \
-    }                                                                                      \
-    _Pragma("unroll") for (int i = 0; i < 4; ++i) {                                        \
-      TG_SG(0x010, 1);                                                                     \
-      TG_SG(0x008, 2);                                                                     \
+    if constexpr (M == 0) {                                                                \
+      _Pragma("unroll") for (int i = 0; i < 8; ++i) { TG_DM; }                             \
+      _Pragma("unroll") for (int i = 0; i < 4; ++i) { TG_SG(0x010, 1); TG_SG(0x008, 2); }  \
+    } else if constexpr (M == 1) {                                                         \
+      _Pragma("unroll") for (int i = 0; i < 6; ++i) { TG_DM; }                             \
+      _Pragma("unroll") for (int i = 0; i < 2; ++i) { TG_SG(0x010, 1); TG_SG(0x008, 1); }  \
+      TG_SG(0x010, 2);                                                                     \
+    } else {                                                                               \
+      _Pragma("unroll") for (int i = 0; i < 4; ++i) { TG_DM; }                             \
+      TG_SG(0x010, 4);                                                                     \
     }                                                                                      \
   } while (0)
-#define TG_PATTERN_LOADS_HALF                                                              \
+    // Sub-step 3 before the barrier: half of the MFMAs with the last 4 loads.
+#define TG_PATTERN_PRE                                                                     \
   do {                                                                                     \
-    _Pragma("unroll") for (int i = 0; i < 4; ++i) {                                        \
-      TG_SG(0x008, 1);                                                                     \
-      TG_SG(0x010, 1);                                                                     \
-      TG_SG(0x008, 1);                                                                     \
+    if constexpr (M == 0) {                                                                \
+      _Pragma("unroll") for (int i = 0; i < 4; ++i) {                                      \
+        TG_SG(0x008, 1); TG_SG(0x010, 1); TG_SG(0x008, 1);                                 \
+      }                                                                                    \
+    } else if constexpr (M == 1) {                                                         \
+      _Pragma("unroll") for (int i = 0; i < 4; ++i) { TG_SG(0x008, 1); TG_SG(0x010, 1); }  \
+    } else {                                                                               \
+      _Pragma("unroll") for (int i = 0; i < 2; ++i) { TG_SG(0x008, 1); TG_SG(0x010, 2); }  \
     }                                                                                      \
   } while (0)
-#define TG_PATTERN_FRAGS(nm)                                                               \
+    // After the barrier: the next stage's first fragment reads with the
+    // other half of the MFMAs.
+#define TG_PATTERN_POST                                                                    \
   do {                                                                                     \
-    _Pragma("unroll") for (int i = 0; i < 8; ++i) {                                        \
-      TG_SG(0x100, 1);                                                                     \
-      TG_SG(0x008, (nm) / 8);                                                              \
-    }                                                                                      \
+    _Pragma("unroll") for (int i = 0; i < NQ / 2; ++i) { TG_DM; }                          \
+    if constexpr (ND > NQ / 2) TG_SG(0x100, ND - NQ / 2);                                  \
   } while (0)
+
+    // A of stage kt+1 and B of stage kt+2 go into the buffers released at
+    // the previous barrier: this tile's, else the next tile's, else (no next
+    // tile) this tile's last stage again.
+#define TG_TARGETS(kt)                                                                     \
+  const bool ca = (kt) + 1 < nk, cb = (kt) + 2 < nk;                                       \
+  const int ka = ca ? (kt) + 1 : (has_n ? (kt) + 1 - nk : nk - 1);                         \
+  const int kb = cb ? (kt) + 2 : (has_n ? (kt) + 2 - nk : nk - 1);                         \
+  const bool a_here = ca || !has_n;                                                        \
+  const __amdgpu_buffer_rsrc_t ra = a_here ? a_cur : a_n;                                  \
+  const __amdgpu_buffer_rsrc_t rb = (cb || !has_n) ? b_cur : b_n;                          \
+  int offa[AI];                                                                            \
+  _Pragma("unroll") for (int i = 0; i < AI; ++i) offa[i] = a_here ? a_off[i] : a_off_n[i]; \
+  const int abn = ab ^ 1, bbn = (bb == 0) ? 2 : bb - 1
 
     int slot, row0, rows, nt;
     seek(L, slot, row0, rows, nt);
@@ -615,116 +633,117 @@ __global__ __launch_bounds__(256) void grouped_gemm_persistent4_kernel(
     if (has_n) seek(Ln, slot_n, row0_n, rows_n, nt_n);
     __amdgpu_buffer_rsrc_t a_n = a_of(row0_n, rows_n), b_n = b_of(slot_n, nt_n);
     a_offsets(row0_n, rows_n, a_off_n);
+    int ab = 0, bb = 0;  // buffers of the current stage
 
-    // Prologue: A and B of stage 0, B of stage 1; stage 0 visible; its first
-    // fragments read.
+    // One tile in mode M (0 full, 1 half, 2 quarter): its K loop and epilogue.
+    // The tile's stage 0 has landed and is visible (previous barrier).
+    auto run_tile = [&](auto mode) __attribute__((always_inline)) {
+      constexpr int M = decltype(mode)::value;
+      constexpr int MBm = (M == 2) ? 2 : 4;  // 32-row blocks per wave
+      constexpr int NBm = (M == 0) ? 4 : 2;  // 32-column blocks per wave
+      constexpr int NQ = MBm * NBm;          // MFMAs per sub-step
+      constexpr int ND = MBm + NBm;          // fragment reads per sub-step
+      const int rbase = (M == 0) ? wm * 128 : 0;
+      const int cw = (M == 0) ? (SWIGLU ? wn * 64 : wn * 128) : (SWIGLU ? wave * 32 : wave * 64);
+      const int xrow = rbase + (lane & 31), wrow = cw + (lane & 31);
+      int xoff[KK], woff[KK];
+#pragma unroll
+      for (int kk = 0; kk < KK; ++kk) {
+        xoff[kk] = xrow * BK + (((2 * kk + khalf) ^ swz<CH>(xrow)) << 3);
+        woff[kk] = 2 * A_ST + wrow * BK + (((2 * kk + khalf) ^ swz<CH>(wrow)) << 3);
+      }
+      // Weight rows of block nb relative to wrow (gate blocks, then up blocks).
+      auto wblk = [](int nb) constexpr {
+        return SWIGLU ? ((nb < NBm / 2) ? nb * 32 : BN / 2 + (nb - NBm / 2) * 32) : nb * 32;
+      };
+      bf16x8 xf[2][MBm], wf[2][NBm];
+      f32x16 acc[NBm][MBm];
+#pragma unroll
+      for (int nb = 0; nb < NBm; ++nb)
+#pragma unroll
+        for (int mb = 0; mb < MBm; ++mb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) acc[nb][mb][r] = 0.0f;
+      // One stage; the last stage of the tile reads no fragments after its
+      // barrier (the next tile may run in another mode).
+#define TG_STAGE(kt, LAST)                                                                 \
+  do {                                                                                     \
+    TG_TARGETS(kt);                                                                        \
+    TG_FRAGS(ab, bb, 1, 1);                                                                \
+    TG_ISSUE_A(ra, offa, ka * BK, abn, 0, AI / 2);                                         \
+    TG_MFMAS(0, 0, NQ);                                                                    \
+    TG_PATTERN_LOADS;                                                                      \
+    __builtin_amdgcn_sched_barrier(0);                                                     \
+    TG_FRAGS(ab, bb, 2, 0);                                                                \
+    TG_ISSUE_A(ra, offa, ka * BK, abn, AI / 2, AI);                                        \
+    TG_MFMAS(1, 0, NQ);                                                                    \
+    TG_PATTERN_LOADS;                                                                      \
+    __builtin_amdgcn_sched_barrier(0);                                                     \
+    TG_FRAGS(ab, bb, 3, 1);                                                                \
+    TG_ISSUE_B(rb, kb * BK, bbn, 0, BI / 2);                                               \
+    TG_MFMAS(0, 0, NQ);                                                                    \
+    TG_PATTERN_LOADS;                                                                      \
+    __builtin_amdgcn_sched_barrier(0);                                                     \
+    __builtin_amdgcn_s_waitcnt(0xc07f); /* lgkmcnt(0): this stage's buffers are read */    \
+    TG_ISSUE_B(rb, kb * BK, bbn, BI / 2, BI);                                              \
+    TG_MFMAS(1, 0, NQ / 2);                                                                \
+    TG_PATTERN_PRE;                                                                        \
+    __builtin_amdgcn_sched_barrier(0);                                                     \
+    TG_WAIT_VM(BI);                                                                        \
+    block_barrier();                                                                       \
+    ab ^= 1;                                                                               \
+    bb = (bb == 2) ? 0 : bb + 1;                                                           \
+    if constexpr (!(LAST)) {                                                               \
+      TG_FRAGS(ab, bb, 0, 0);                                                              \
+      TG_MFMAS(1, NQ / 2, NQ);                                                             \
+      TG_PATTERN_POST;                                                                     \
+    } else {                                                                               \
+      TG_MFMAS(1, NQ / 2, NQ);                                                             \
+    }                                                                                      \
+    __builtin_amdgcn_sched_barrier(0);                                                     \
+  } while (0)
+      TG_FRAGS(ab, bb, 0, 0);
+      for (int kt = 0; kt < nk - 1; ++kt) TG_STAGE(kt, false);
+      TG_STAGE(nk - 1, true);
+#undef TG_STAGE
+      // acc[nb][mb] register r of lane l: row mb*32 + l%32, column
+      // nb*32 + 8*(r/4) + 4*(l/32) + r%4 of the wave's sub-tile; SwiGLU pairs
+      // gate block nb with up block nb + NBm/2.
+      const int colbase = SWIGLU ? nt * (BN / 2) + cw : nt * BN + cw;
+#pragma unroll
+      for (int mb = 0; mb < MBm; ++mb) {
+        const int r = rbase + mb * 32 + (lane & 31);
+        uint16_t* crow = C + (size_t)(row0 + r) * ldc + colbase + 4 * (lane >> 5);
+#pragma unroll
+        for (int nb = 0; nb < (SWIGLU ? NBm / 2 : NBm); ++nb) {
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            float v[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              const int rr = 4 * q + e;
+              v[e] = SWIGLU ? swiglu(acc[nb][mb][rr], acc[nb + NBm / 2][mb][rr]) : acc[nb][mb][rr];
+            }
+            uint2 pk;
+            pk.x = pack_bf16x2(v[0], v[1]);
+            pk.y = pack_bf16x2(v[2], v[3]);
+            if (r < rows) *reinterpret_cast<uint2*>(crow + nb * 32 + 8 * q) = pk;
+          }
+        }
+      }
+    };
+
+    // Prologue: A and B of stage 0, B of stage 1; stage 0 visible.
     TG_ISSUE_A(a_cur, a_off, 0, 0, 0, AI);
     TG_ISSUE_B(b_cur, 0, 0, 0, BI);
     TG_ISSUE_B(b_cur, BK, 1, 0, BI);
     TG_WAIT_VM(BI);
     block_barrier();
-    TG_FRAGS(0, 0, 0, 0);
 
-    int ab = 0, bb = 0;  // buffers of the current stage
     for (;;) {
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-        for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) acc[nb][mb][r] = 0.0f;
-      const bool active = wm * (BM / WM) < rows;
-      // A of stage kt+1 and B of stage kt+2 go into the buffers released at
-      // the previous barrier: this tile's, else the next tile's, else (no
-      // next tile) this tile's last stage again.
-#define TG_TARGETS(kt)                                                                     \
-  const bool ca = (kt) + 1 < nk, cb = (kt) + 2 < nk;                                       \
-  const int ka = ca ? (kt) + 1 : (has_n ? (kt) + 1 - nk : nk - 1);                         \
-  const int kb = cb ? (kt) + 2 : (has_n ? (kt) + 2 - nk : nk - 1);                         \
-  const bool a_here = ca || !has_n;                                                        \
-  const __amdgpu_buffer_rsrc_t ra = a_here ? a_cur : a_n;                                  \
-  const __amdgpu_buffer_rsrc_t rb = (cb || !has_n) ? b_cur : b_n;                          \
-  int offa[AI];                                                                            \
-  _Pragma("unroll") for (int i = 0; i < AI; ++i) offa[i] = a_here ? a_off[i] : a_off_n[i]; \
-  const int abn = ab ^ 1, bbn = (bb == 0) ? 2 : bb - 1
-      if (active) {
-        for (int kt = 0; kt < nk; ++kt) {
-          TG_TARGETS(kt);
-          TG_FRAGS(ab, bb, 1, 1);
-          TG_ISSUE_A(ra, offa, ka * BK, abn, 0, AI / 2);
-          TG_MFMAS(0, 0, 16);
-          TG_PATTERN_LOADS;
-          __builtin_amdgcn_sched_barrier(0);
-          TG_FRAGS(ab, bb, 2, 0);
-          TG_ISSUE_A(ra, offa, ka * BK, abn, AI / 2, AI);
-          TG_MFMAS(1, 0, 16);
-          TG_PATTERN_LOADS;
-          __builtin_amdgcn_sched_barrier(0);
-          TG_FRAGS(ab, bb, 3, 1);
-          TG_ISSUE_B(rb, kb * BK, bbn, 0, BI / 2);
-          TG_MFMAS(0, 0, 16);
-          TG_PATTERN_LOADS;
-          __builtin_amdgcn_sched_barrier(0);
-          __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this stage's buffers are read
-          TG_ISSUE_B(rb, kb * BK, bbn, BI / 2, BI);
-          TG_MFMAS(1, 0, 8);
-          TG_PATTERN_LOADS_HALF;
-          __builtin_amdgcn_sched_barrier(0);
-          TG_WAIT_VM(BI);
-          block_barrier();
-          ab ^= 1;
-          bb = (bb == 2) ? 0 : bb + 1;
-          TG_FRAGS(ab, bb, 0, 0);
-          TG_MFMAS(1, 8, 16);
-          TG_PATTERN_FRAGS(8);
-          __builtin_amdgcn_sched_barrier(0);
-        }
-      } else {
-        __builtin_amdgcn_s_waitcnt(0xc07f);  // fragment reads of the previous tile
-        for (int kt = 0; kt < nk; ++kt) {
-          TG_TARGETS(kt);
-          TG_ISSUE_A(ra, offa, ka * BK, abn, 0, AI);
-          TG_ISSUE_B(rb, kb * BK, bbn, 0, BI);
-          TG_WAIT_VM(BI);
-          block_barrier();
-          ab ^= 1;
-          bb = (bb == 2) ? 0 : bb + 1;
-        }
-        TG_FRAGS(ab, bb, 0, 0);
-      }
-#undef TG_TARGETS
-      // acc[nb][mb] register r of lane l: row mb*32 + l%32, column
-      // nb*32 + 8*(r/4) + 4*(l/32) + r%4 of the wave's sub-tile.
-      if (active) {
-        const int colbase = SWIGLU ? nt * (BN / 2) + wn * WOUT : nt * BN + wn * WOUT;
-#pragma unroll
-        for (int mb = 0; mb < MB; ++mb) {
-          const int r = wm * (BM / WM) + mb * 32 + (lane & 31);
-          uint16_t* crow = C + (size_t)(row0 + r) * ldc + colbase + 4 * (lane >> 5);
-#pragma unroll
-          for (int nb = 0; nb < (SWIGLU ? NB / 2 : NB); ++nb) {
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-              float v[4];
-#pragma unroll
-              for (int e = 0; e < 4; ++e) {
-                const int rr = 4 * q + e;
-                if (SWIGLU) {
-                  const float g = acc[nb][mb][rr];
-                  const float u = acc[nb + NB / 2][mb][rr];
-                  v[e] = swiglu(g, u);
-                } else {
-                  v[e] = acc[nb][mb][rr];
-                }
-              }
-              uint2 pk;
-              pk.x = pack_bf16x2(v[0], v[1]);
-              pk.y = pack_bf16x2(v[2], v[3]);
-              if (r < rows) *reinterpret_cast<uint2*>(crow + nb * 32 + 8 * q) = pk;
-            }
-          }
-        }
-      }
+      if (rows > 128) run_tile(std::integral_constant<int, 0>{});
+      else if (rows > 64) run_tile(std::integral_constant<int, 1>{});
+      else run_tile(std::integral_constant<int, 2>{});
       if (!has_n) break;
       row0 = row0_n;
       rows = rows_n;
@@ -743,9 +762,11 @@ __global__ __launch_bounds__(256) void grouped_gemm_persistent4_kernel(
       }
     }
     TG_WAIT_VM(0);  // no LDS write may land after the walk
-#undef TG_PATTERN_FRAGS
-#undef TG_PATTERN_LOADS_HALF
+#undef TG_TARGETS
+#undef TG_PATTERN_POST
+#undef TG_PATTERN_PRE
 #undef TG_PATTERN_LOADS
+#undef TG_DM
 #undef TG_SG
 #undef TG_FRAGS
 #undef TG_MFMAS
