@@ -234,13 +234,105 @@ __global__ __launch_bounds__(256) void logits_topk_kernel(const float* __restric
   wave_topk_any(lg, E, k, t, ids, w);
 }
 
+// Logits mode for E <= 256 and k <= 16: four tokens per wave, one 16-lane
+// DPP row per token. Lane l of a row holds the candidates l, l + 16, ... of
+// its token in registers as 64-bit keys: the float32 logit in an order-
+// preserving encoding (-0 taken as +0) above the complement of the expert
+// id, so a larger key is a larger logit or, on equal logits, a lower id, and
+// no two keys are equal. Round j takes every lane's largest key below the
+// previous winner's and reduces the row with the four DPP row steps, so
+// every lane of the row knows each round's winner (no lane reads, no LDS).
+// Lane j keeps the j-th winner; every lane sums the k exponentials in rank
+// order, the same sum as the one-token-per-wave kernel.
+constexpr int kRowTokens = 4;  // tokens per wave
+
+__device__ __forceinline__ uint64_t topk_key(float v, int e) {
+  uint32_t u = __float_as_uint(v == 0.0f ? 0.0f : v);
+  u = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+  return ((uint64_t)u << 32) | (0xffffffffu - (uint32_t)e);
+}
+
+__device__ __forceinline__ float key_value(uint64_t key) {
+  const uint32_t u = (uint32_t)(key >> 32);
+  return __uint_as_float((u & 0x80000000u) ? (u & 0x7fffffffu) : ~u);
+}
+
+__device__ __forceinline__ uint64_t row_max_key(uint64_t k) {
+#define TG_DPP_MAX(ctrl)                                                                  \
+  do {                                                                                    \
+    const uint32_t lo = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)k, ctrl, 0xF, 0xF,   \
+                                                    false);                               \
+    const uint32_t hi = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)(k >> 32), ctrl,     \
+                                                    0xF, 0xF, false);                     \
+    const uint64_t o = ((uint64_t)hi << 32) | lo;                                         \
+    k = o > k ? o : k;                                                                    \
+  } while (0)
+  TG_DPP_MAX(0xB1);   // quad_perm [1,0,3,2]
+  TG_DPP_MAX(0x4E);   // quad_perm [2,3,0,1]
+  TG_DPP_MAX(0x141);  // row_half_mirror
+  TG_DPP_MAX(0x140);  // row_mirror
+#undef TG_DPP_MAX
+  return k;
+}
+
+template <int NQ>
+__global__ __launch_bounds__(256) void logits_topk_rows_kernel(const float* __restrict__ logits,
+                                                               int T, int E, int k,
+                                                               int32_t* __restrict__ ids,
+                                                               float* __restrict__ w) {
+  const int lane = lane_id();
+  const int l16 = lane & 15;
+  const int t = (blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave) * kRowTokens + (lane >> 4);
+  const bool on = t < T;
+  uint64_t key[NQ];
+#pragma unroll
+  for (int q = 0; q < NQ; ++q) {
+    const int e = l16 + 16 * q;
+    key[q] = (on && e < E) ? topk_key(logits[(size_t)t * E + e], e) : 0;  // 0: no candidate
+  }
+  uint64_t thr = ~0ull;
+  float my_v = 0.0f, v0 = 0.0f, z = 0.0f;
+  int my_id = 0;
+  for (int j = 0; j < k; ++j) {
+    uint64_t best = 0;
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) best = (key[q] < thr && key[q] > best) ? key[q] : best;
+    best = row_max_key(best);  // every lane of the row: this round's winner
+    thr = best;
+    const float bv = key_value(best);
+    if (j == 0) v0 = bv;
+    const float ex = expf(bv - v0);
+    z += ex;
+    if (l16 == j) {
+      my_v = ex;
+      my_id = (int)(0xffffffffu - (uint32_t)best);
+    }
+  }
+  if (on && l16 < k) {
+    ids[(size_t)t * k + l16] = my_id;
+    w[(size_t)t * k + l16] = my_v / z;
+  }
+}
+
 }  // namespace
 
 hipError_t launch_gate_topk(const uint16_t* x, const uint16_t* wg, const float* logits_in, int T,
                             int d, int E, int k, float* logits_out, int32_t* ids, float* w,
                             hipStream_t stream) {
   if (T == 0) return hipSuccess;
-  if (logits_in) {
+  if (logits_in && E <= 256 && k <= 16 && T >= 4096) {
+    const int per_block = 4 * kRowTokens;  // 4 waves of 4 tokens
+    const dim3 grid((T + per_block - 1) / per_block);
+    if (E <= 64)
+      hipLaunchKernelGGL(logits_topk_rows_kernel<4>, grid, dim3(256), 0, stream, logits_in, T, E, k,
+                         ids, w);
+    else if (E <= 128)
+      hipLaunchKernelGGL(logits_topk_rows_kernel<8>, grid, dim3(256), 0, stream, logits_in, T, E, k,
+                         ids, w);
+    else
+      hipLaunchKernelGGL(logits_topk_rows_kernel<16>, grid, dim3(256), 0, stream, logits_in, T, E,
+                         k, ids, w);
+  } else if (logits_in) {
     hipLaunchKernelGGL(logits_topk_kernel, dim3((T + kWaves - 1) / kWaves), dim3(256), 0, stream,
                        logits_in, T, E, k, ids, w);
   } else if ((long)E * d <= kStageElems && E <= kStagedMaxE) {

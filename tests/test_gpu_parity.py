@@ -194,6 +194,31 @@ def test_repeat_calls_are_bit_identical(tiny):
         assert np.array_equal(np.asarray(a[key]), np.asarray(b[key])), key
 
 
+@pytest.mark.parametrize("T,E,k", [(64, 64, 8), (64, 256, 16), (5000, 64, 8), (5000, 200, 1),
+                                   (5000, 256, 8), (4096, 256, 16), (4100, 130, 5)])
+def test_logits_topk_ties_and_signed_zeros(T, E, k):
+    """Logits mode with many equal logits (including -0 next to +0 and whole
+    rows of one value): ids must follow (larger first, equal -> lower id)
+    exactly, weights within 1e-6, for small batches (one token per wave) and
+    large ones (four tokens per wave)."""
+    print(f"[gpu] top-k ties T={T} E={E} k={k}", flush=True)
+    rng = np.random.default_rng(T * 7 + E * 3 + k)
+    vals = np.array([-2.0, -0.5, -0.0, 0.0, 0.25, 1.0, 3.0], dtype=np.float32)
+    logits = vals[rng.integers(0, len(vals), size=(T, E))]
+    logits[::17] = 0.25                      # rows of one value
+    logits[5::23, : E // 2] = -0.0           # -0 and +0 side by side
+    logits[5::23, E // 2:] = 0.0
+    lg = torch.from_numpy(logits).to(DEV)
+    ids = torch.empty((T, k), dtype=torch.int32, device=DEV)
+    w = torch.empty((T, k), dtype=torch.float32, device=DEV)
+    tg.tg_gate_topk(None, None, lg, T, 256, E, k, None, ids, w)
+    torch.cuda.synchronize()
+    ref_ids = O.topk(logits, k)
+    assert np.array_equal(host(ids), ref_ids), "top-k ids differ from the oracle"
+    ref_w = O.gate_weights(logits, ref_ids)
+    assert np.abs(host(w).astype(np.float64) - ref_w).max() <= G.W_ATOL
+
+
 # ---------------------------------------------------------------- random shapes and edge cases
 
 RANDOM_CASES = [
