@@ -9,10 +9,14 @@
 //      batch of §5.2) get slot -2 and are not counted. In replay mode (§5.1)
 //      a pair keeps its first-pass slot while that slot is alive and is
 //      otherwise given its first live candidate now, to be recomputed;
-//   2. scan: per-slot totals, exclusive slot offsets, and the base row of
-//      every (chunk, slot) in chunk order;
+//   2. scan: per-slot totals, exclusive slot offsets, and the position of
+//      every (chunk, slot) within its slot in chunk order (the histograms
+//      are slot-major, so one wave scans one slot's chunks);
 //   3. scatter: each wave walks an equal share of a chunk in pair order and
-//      ranks equal slots with ballots, so rows follow (slot, token, rank).
+//      ranks the pairs of each group of 64 by slot: one ballot per bit of
+//      the slot index gives every lane the lanes that share its slot, so the
+//      rank costs the same for any mix of slots, and rows follow
+//      (slot, token, rank).
 // Up to 2048 pairs, one block runs all three passes (the batch of a decode
 // step fits, and two launches are saved).
 // The gather then copies one activation row per routed pair with 16-byte
@@ -92,73 +96,84 @@ __global__ __launch_bounds__(kBlock) void remap_count_kernel(
     if (slot >= 0) atomicAdd(&h[slot], 1);
   }
   __syncthreads();
-  for (int s = threadIdx.x; s < S; s += kBlock) hist[(size_t)blockIdx.x * S + s] = h[s];
+  for (int s = threadIdx.x; s < S; s += kBlock) hist[(size_t)s * gridDim.x + blockIdx.x] = h[s];
   if (threadIdx.x == 0) unserved_chunk[blockIdx.x] = nu;
 }
 
-// One block of 1024 threads; thread s owns slot s.
+// One block of 1024 threads (16 waves). hist[s * nchunks + c] holds the
+// pairs of chunk c on slot s (nchunks <= 4 * 64). Wave w takes slots w,
+// w + 16, ...: lane l sums chunks 4l .. 4l+3, a wave scan gives every chunk
+// its exclusive position within the slot (written back in place, the
+// scatter adds the slot offset), and the slot totals go through a block
+// scan to the exclusive slot offsets.
 __global__ __launch_bounds__(1024) void scan_kernel(int32_t* __restrict__ hist,
                                                     const int32_t* __restrict__ unserved_chunk,
                                                     int nchunks, int S, int32_t* __restrict__ counts,
                                                     int32_t* __restrict__ offsets,
                                                     int32_t* __restrict__ n_unserved,
                                                     int32_t* __restrict__ total_out) {
+  __shared__ int tot[1024];
   __shared__ int sc[2][1024];
   __shared__ int nu;
-  const int s = threadIdx.x;
-  if (s == 0) nu = 0;
-  int total = 0;
-  if (s < S) {
-    // Loads of 8 chunks are issued together; the running sum is sequential.
-    for (int c0 = 0; c0 < nchunks; c0 += 8) {
-      int v[8];
+  const int tid = threadIdx.x;
+  const int wave = tid / kWave, lane = lane_id();
+  if (tid == 0) nu = 0;
+  for (int s = wave; s < S; s += 1024 / kWave) {
+    int32_t* hs = hist + (size_t)s * nchunks;
+    int v[4], sum = 0;
 #pragma unroll
-      for (int i = 0; i < 8; ++i) v[i] = (c0 + i < nchunks) ? hist[(size_t)(c0 + i) * S + s] : 0;
-#pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        if (c0 + i < nchunks) hist[(size_t)(c0 + i) * S + s] = total;  // made absolute below
-        total += v[i];
-      }
+    for (int i = 0; i < 4; ++i) {
+      const int c = 4 * lane + i;
+      v[i] = (c < nchunks) ? hs[c] : 0;
+      sum += v[i];
     }
+    int incl = sum;
+#pragma unroll
+    for (int off = 1; off < kWave; off <<= 1) {
+      const int t = __shfl_up(incl, off);
+      if (lane >= off) incl += t;
+    }
+    int run = incl - sum;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int c = 4 * lane + i;
+      if (c < nchunks) hs[c] = run;
+      run += v[i];
+    }
+    if (lane == kWave - 1) tot[s] = incl;
   }
   int part = 0;
-  for (int c = s; c < nchunks; c += 1024) part += unserved_chunk[c];
-  sc[0][s] = (s < S) ? total : 0;
+  for (int c = tid; c < nchunks; c += 1024) part += unserved_chunk[c];
   __syncthreads();
   if (part) atomicAdd(&nu, part);
   // Hillis-Steele inclusive scan over the slot totals.
+  const int total = (tid < S) ? tot[tid] : 0;
+  sc[0][tid] = total;
+  __syncthreads();
   int cur = 0;
   for (int off = 1; off < 1024; off <<= 1) {
-    const int v = sc[cur][s] + (s >= off ? sc[cur][s - off] : 0);
-    sc[cur ^ 1][s] = v;
+    sc[cur ^ 1][tid] = sc[cur][tid] + (tid >= off ? sc[cur][tid - off] : 0);
     cur ^= 1;
     __syncthreads();
   }
-  const int incl = sc[cur][s];
-  const int excl = incl - ((s < S) ? total : 0);
-  if (s < S) {
-    counts[s] = total;
-    offsets[s] = excl;
-    for (int c0 = 0; c0 < nchunks; c0 += 8) {
-      int v[8];
-#pragma unroll
-      for (int i = 0; i < 8; ++i) v[i] = (c0 + i < nchunks) ? hist[(size_t)(c0 + i) * S + s] : 0;
-#pragma unroll
-      for (int i = 0; i < 8; ++i)
-        if (c0 + i < nchunks) hist[(size_t)(c0 + i) * S + s] = v[i] + excl;
-    }
+  const int incl = sc[cur][tid];
+  if (tid < S) {
+    counts[tid] = total;
+    offsets[tid] = incl - total;
   }
-  if (s == S - 1) {
+  if (tid == S - 1) {
     offsets[S] = incl;
     if (total_out) total_out[0] = incl;
   }
-  __syncthreads();
-  if (s == 0) n_unserved[0] = nu;
+  if (tid == 0) n_unserved[0] = nu;
 }
 
+// rel[s * nchunks + c]: position of chunk c's first pair within slot s
+// (from scan_kernel); sbits: bits of the largest slot index.
 __global__ __launch_bounds__(kBlock) void scatter_kernel(const int32_t* __restrict__ pair_slot,
-                                                         int npairs, int S,
-                                                         const int32_t* __restrict__ base,
+                                                         int npairs, int S, int nchunks, int sbits,
+                                                         const int32_t* __restrict__ rel,
+                                                         const int32_t* __restrict__ offsets,
                                                          int32_t* __restrict__ perm,
                                                          int32_t* __restrict__ pair_row,
                                                          int chunk) {
@@ -180,7 +195,7 @@ __global__ __launch_bounds__(kBlock) void scatter_kernel(const int32_t* __restri
   }
   __syncthreads();
   for (int s = threadIdx.x; s < S; s += kBlock) {
-    int run = base[(size_t)blockIdx.x * S + s];
+    int run = offsets[s] + rel[(size_t)s * nchunks + blockIdx.x];
     for (int w = 0; w < kWaves; ++w) {
       const int v = cnt[w][s];
       cnt[w][s] = run;
@@ -196,19 +211,23 @@ __global__ __launch_bounds__(kBlock) void scatter_kernel(const int32_t* __restri
       s = pair_slot[p];
       if (s < 0) pair_row[p] = -1;
     }
-    uint64_t active = __ballot(s >= 0);
-    while (active) {
-      const int leader = __builtin_ctzll(active);
-      const int sl = __shfl(s, leader);
-      const uint64_t m = __ballot(s == sl) & active;
-      const int start = cnt[wave][sl];
-      if (s == sl) {
-        const int row = start + __builtin_popcountll(m & lt);
-        perm[row] = p;
-        pair_row[p] = row;
-      }
-      if (lane == leader) cnt[wave][sl] = start + __builtin_popcountll(m);
-      active &= ~m;
+    // Lanes holding a routed pair whose slot equals this lane's: start from
+    // the routed lanes and keep, for every bit of the slot index, the lanes
+    // that agree with this lane on that bit.
+    uint64_t eq = __ballot(s >= 0);
+    if (!eq) continue;  // uniform
+    for (int b = 0; b < sbits; ++b) {
+      const bool bit = (s >> b) & 1;
+      const uint64_t mb = __ballot(bit);
+      eq &= bit ? mb : ~mb;
+    }
+    if (s >= 0) {
+      const int row = cnt[wave][s] + __builtin_popcountll(eq & lt);
+      perm[row] = p;
+      pair_row[p] = row;
+      // The slot's lowest lane advances the slot's next row (every lane's
+      // read above precedes this write in the wave's LDS order).
+      if (!(eq & lt)) cnt[wave][s] = row + __builtin_popcountll(eq);
     }
   }
 }
@@ -390,8 +409,9 @@ hipError_t remap_dispatch(bool replay, const int32_t* ids, int T, int k, const i
   hipLaunchKernelGGL(scan_kernel, dim3(1), dim3(1024), 0, stream, hist, unserved_chunk, nchunks, S,
                      counts, offsets, n_unserved, total_out);
   if (nchunks > 0) {
+    const int sbits = (S > 1) ? 32 - __builtin_clz((unsigned)(S - 1)) : 0;
     hipLaunchKernelGGL(scatter_kernel, dim3(nchunks), dim3(kBlock), 0, stream, pair_slot, npairs, S,
-                       hist, perm, pair_row, chunk);
+                       nchunks, sbits, hist, offsets, perm, pair_row, chunk);
     if (x_perm) {
       const int nch = d / 8;
       const long maxq = (long)npairs * nch;

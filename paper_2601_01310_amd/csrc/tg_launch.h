@@ -14,10 +14,10 @@ hipError_t launch_gate_topk(const uint16_t* x, const uint16_t* wg, const float* 
                             int d, int E, int k, float* logits_out, int32_t* ids, float* w,
                             hipStream_t stream);
 
-// Pairs are processed in about kDispatchChunks chunks (each a multiple of
+// Pairs are processed in at most kDispatchChunks chunks (each a multiple of
 // 256 pairs, at least 256); the workspace holds one S-wide histogram and one
 // unserved count per chunk.
-constexpr int kDispatchChunks = 64;
+constexpr int kDispatchChunks = 256;
 int dispatch_chunk(long npairs);
 size_t dispatch_workspace_bytes(int T, int k, int S);
 // token_valid (optional, [T]): pairs of tokens with 0 get pair_slot -2 and
