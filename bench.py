@@ -23,7 +23,8 @@ PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 RIDGE_FLOP_PER_BYTE = PEAK_BF16_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9)
 STAGES = ["gate", "dispatch", "ffn_gateup", "ffn_down", "combine"]
-GEMM_SRC = os.path.join(ROOT, "paper_2601_01310_amd", "csrc", "grouped_gemm.hip")
+GEMM_SRC = [os.path.join(ROOT, "paper_2601_01310_amd", "csrc", f)
+            for f in ("grouped_gemm.hip", "tg_device.h")]
 TRAFFIC = os.path.join(ROOT, "profiles", "gemm_gateup_mixtral_traffic.json")
 
 
@@ -36,7 +37,7 @@ def measured_traffic(workload: str):
         rec = json.load(open(TRAFFIC))
     except (OSError, ValueError):
         return None
-    sha = hashlib.sha256(open(GEMM_SRC, "rb").read()).hexdigest()
+    sha = hashlib.sha256(b"".join(open(f, "rb").read() for f in GEMM_SRC)).hexdigest()
     if rec.get("source_sha256") != sha or rec.get("workload") != workload:
         return None
     return rec.get("traffic_bytes_per_dispatch")
@@ -76,7 +77,7 @@ class HipEvents:
             self.hip.hipEventDestroy(ctypes.c_void_p(e))
 
 
-def cpu_baseline(wl, n_tokens: int = 1024):
+def cpu_baseline(wl, n_tokens: int = 1536):
     """The CPU oracle, as it stands, on a bounded sample of the workload:
     the full forward of ``n_tokens`` seeded tokens (their routed pairs)."""
     import numpy as np
