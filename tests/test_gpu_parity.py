@@ -258,6 +258,31 @@ def test_random_shapes_match_oracle(case):
         assert np.array_equal(f["out"], g["out"]), "fused differs from stepwise"
 
 
+@pytest.mark.parametrize("gate,T", [("logits", 200), ("weights", 64)])
+def test_largest_supported_shapes_match_oracle(gate, T):
+    """The ABI's limits: E = 1024 experts, k = 32, S = 1024 slots (1000
+    primaries and 24 shadows: slot indices need 10 bits), routing exact and
+    outputs within tolerance, with and without a quarter of the slots
+    failed."""
+    print(f"[gpu] largest shapes gate={gate} T={T}", flush=True)
+    shadows = list(range(0, 1000, 42))[:24]
+    wl = synth.make_custom(T=T, d=256, E=1024, k=32, I=128, n_local=1000, shadow_experts=shadows,
+                           gate=gate, seed=111, device=DEV)
+    assert wl.S == 1024
+    rng = np.random.default_rng(112)
+    alive = wl.alive.clone()
+    alive[torch.from_numpy(rng.choice(wl.S, size=wl.S // 4, replace=False)).to(DEV)] = 0
+    for al in (wl.alive, alive):
+        g = G.run_stepwise(wl, al)
+        r = _oracle_full(wl, al)
+        if g["logits"] is not None:
+            assert np.array_equal(g["logits"], r["logits"])
+        G.assert_routing_equal(g, r)
+        G.assert_close_bf16(g["out"], r["out"], "out")
+        f = G.run_fused(wl, al)
+        assert np.array_equal(f["out"], g["out"]), "fused differs from stepwise"
+
+
 def test_empty_batch():
     wl = synth.make_custom(T=4, d=256, E=8, k=2, I=128, n_local=8, shadow_experts=[],
                            gate="weights", seed=5, device=DEV)
