@@ -122,14 +122,17 @@ def test_ffn_tile_shapes_give_identical_bits(tiny):
     G.assert_close_bf16(outs[0][1][o:o + 70], ref, "y slot 3")
 
 
-def test_ffn_partial_last_round_split_matches_oracle():
-    """d = 4096 gives the down projection 16 column panels of 256; 17 row
-    blocks of 256 make 272 tiles, so 16 tiles spill past the 256 CUs of one
-    round and run as quarter tiles. Every row is checked against the oracle,
-    and rows of a layout without that spill (the last slot empty: 224
-    tiles) give the same bits."""
+@pytest.mark.parametrize("big", [700, 1700], ids=["spill16", "spill80"])
+def test_ffn_partial_last_round_split_matches_oracle(big):
+    """d = 4096 gives the down projection 16 column panels of 256. With 17
+    row blocks of 256 (272 tiles) 16 tiles spill past the 256 CUs of one
+    round and run as 64 quarter tiles; with 21 row blocks (336 tiles) 80
+    spill into 320 quarters, so some blocks take two. Every row is checked
+    against the oracle, and the rows of a second layout (the last slot
+    empty: 224 tiles without a spill, or 288 tiles with a spill of 32) give
+    the same bits."""
     d, I, S = 4096, 128, 10
-    counts = [300, 256, 1, 513, 0, 200, 255, 257, 700, 530]  # 17 row blocks of 256
+    counts = [300, 256, 1, 513, 0, 200, 255, 257, big, 530]  # 17 or 21 row blocks of 256
     g = torch.Generator().manual_seed(11)
     x = torch.randn((sum(counts), d), generator=g).to(torch.bfloat16).to(DEV)
     w13 = (torch.randn((S, 2 * I, d), generator=g) * 0.02).to(torch.bfloat16).to(DEV)
