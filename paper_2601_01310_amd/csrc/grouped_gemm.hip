@@ -24,7 +24,10 @@
 // which the freed buffers are refilled, and the next stage's first
 // fragments are read while the stage's last MFMAs run. Rows past the end of
 // a group read as zeros through the buffer range check and are never
-// stored; waves whose rows all lie past the end skip their MFMAs.
+// stored; waves whose rows all lie past the end skip their MFMAs. Likewise a
+// slot's last weight panel may be partial (I or d not a multiple of the
+// panel width): its rows past the slot's weights read as zeros and its
+// columns past the output width are never stored.
 //
 // For GEMM1 the weight tile holds BN/2 gate rows and the matching BN/2 up
 // rows and every wave owns equal numbers of both, so g and u of one output
@@ -104,6 +107,15 @@ __device__ __forceinline__ void load_lds16(__amdgpu_buffer_rsrc_t rsrc, lds_u16*
 // Raw buffer resource over [base, base + bytes); loads beyond it return 0.
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+
+// Resource over the weight rows b_row0 .. end of slot `slot` (NW rows of K
+// elements per slot); empty when b_row0 lies past the slot's last row.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t weight_rsrc(const uint16_t* B, int slot, int NW,
+                                                              size_t b_row0, int K) {
+  const size_t end = (size_t)(slot + 1) * NW;
+  const size_t bytes = b_row0 < end ? (end - b_row0) * K * 2 : 0;
+  return make_rsrc(B + b_row0 * K, (uint32_t)min((size_t)0x7fffffff, bytes));
 }
 
 struct TileInfo {
@@ -230,8 +242,7 @@ __device__ __forceinline__ void gemm_tile(uint16_t* smem, const TileInfo& tile,
   const __amdgpu_buffer_rsrc_t a_rsrc =
       GATHER ? make_rsrc(A, (uint32_t)A_rows * K * 2)
              : make_rsrc(A + (size_t)row0 * K, (uint32_t)rows * K * 2);
-  const __amdgpu_buffer_rsrc_t b_rsrc = make_rsrc(
-      B + b_row0 * K, (uint32_t)min((size_t)0x7fffffff, ((size_t)(slot + 1) * NW - b_row0) * K * 2));
+  const __amdgpu_buffer_rsrc_t b_rsrc = weight_rsrc(B, slot, NW, b_row0, K);
   int a_off[AI], b_off[BI];  // byte offsets
 #pragma unroll
   for (int i = 0; i < AI; ++i) {
@@ -404,7 +415,7 @@ __device__ __forceinline__ void gemm_tile(uint16_t* smem, const TileInfo& tile,
     for (int i = 0; i < (32 * CPR + kWave - 1) / kWave; ++i) {
       const int q = lane + kWave * i;
       const int r = q / CPR, c = q - r * CPR;
-      if (q < 32 * CPR && mbase + r < rows) {
+      if (q < 32 * CPR && mbase + r < rows && colbase + c * 8 < ldc) {
         *reinterpret_cast<uint4*>(C + (size_t)(row0 + mbase + r) * ldc + colbase + c * 8) =
             *reinterpret_cast<const uint4*>(region + r * WP + c * 8);
       }
@@ -495,8 +506,7 @@ __global__ __launch_bounds__(256) void grouped_gemm_persistent4_kernel(
     };
     auto b_of = [&](int slot, int nt) {
       const size_t b_row0 = (size_t)slot * NW + (SWIGLU ? nt * (BN / 2) : nt * BN);
-      return make_rsrc(B + b_row0 * K,
-                       (uint32_t)min((size_t)0x7fffffff, ((size_t)(slot + 1) * NW - b_row0) * K * 2));
+      return weight_rsrc(B, slot, NW, b_row0, K);
     };
     auto a_of = [&](int row0, int rows) {
       return GATHER ? make_rsrc(A, (uint32_t)A_rows * K * 2)
@@ -727,7 +737,8 @@ __global__ __launch_bounds__(256) void grouped_gemm_persistent4_kernel(
             uint2 pk;
             pk.x = pack_bf16x2(v[0], v[1]);
             pk.y = pack_bf16x2(v[2], v[3]);
-            if (r < rows) *reinterpret_cast<uint2*>(crow + nb * 32 + 8 * q) = pk;
+            if (r < rows && colbase + 4 * (lane >> 5) + nb * 32 + 8 * q < ldc)
+              *reinterpret_cast<uint2*>(crow + nb * 32 + 8 * q) = pk;
           }
         }
       }
@@ -786,7 +797,9 @@ __global__ __launch_bounds__(256) void grouped_gemm_persistent4_kernel(
       m = 2 * m + (q % 4) / 2;
       t.nt = 2 * t.nt + q % 2;
       const int rows = min(BM / 2, t.rows - m * (BM / 2));
-      if (rows > 0) {
+      // A quarter past a partial last panel has no output column to store.
+      const int col0 = t.nt * (SWIGLU ? BN / 4 : BN / 2);
+      if (rows > 0 && col0 < ldc) {
         t.row0 += m * (BM / 2);
         t.rows = rows;
         gemm_tile<BM / 2, BN / 2, BK, 2, 2, SWIGLU, GATHER>(smem, t, A, B, K, NW, I, C, ldc, perm, 1,
@@ -834,7 +847,7 @@ hipError_t launch_grouped(const uint16_t* A, const int32_t* offsets, int S, int 
 }
 
 // Launch of the 4-wave persistent kernel: one block per CU (a multiple of
-// 8); K of at least 2 stages (d is a multiple of 256, I of 128).
+// 8); K of at least 2 stages (d and I are multiples of 64, at least 128).
 template <bool SWIGLU, bool GATHER, bool TAIL>
 hipError_t launch_persistent4(const uint16_t* A, const int32_t* offsets, int S, const uint16_t* B,
                               int K, int NW, int I, uint16_t* C, int ldc, int NT,
@@ -854,16 +867,23 @@ constexpr int kSmallRowsPerSlot = 32;
 
 bool small_batch(int S, int max_rows) { return max_rows <= kSmallRowsPerSlot * (long)S; }
 
+// Weight panels per slot: gate/up panels hold kBN / 2 output columns (as
+// many gate as up rows), down panels kBN. A last, partial panel (I or d not
+// a multiple of the panel width) reads zeros past the slot's weight rows and
+// stores only the columns below the output width.
+int panels_gateup(int I) { return (I + kBN / 2 - 1) / (kBN / 2); }
+int panels_down(int d) { return (d + kBN - 1) / kBN; }
+
 }  // namespace
 
 hipError_t launch_ffn_gateup(const uint16_t* x_perm, const int32_t* offsets, int S, int max_rows,
                              const uint16_t* w13, int d, int I, uint16_t* h, hipStream_t stream) {
   if (max_rows == 0) return hipSuccess;
   if (small_batch(S, max_rows))
-    return launch_grouped<TG_SMALL, true, false>(x_perm, offsets, S, max_rows, w13, d,
-                                                        2 * I, I, h, I, (2 * I) / kBN, stream);
+    return launch_grouped<TG_SMALL, true, false>(x_perm, offsets, S, max_rows, w13, d, 2 * I, I,
+                                                 h, I, panels_gateup(I), stream);
   return launch_persistent4<true, false, false>(x_perm, offsets, S, w13, d, 2 * I, I, h, I,
-                                                (2 * I) / kBN, stream, nullptr, 1, 0);
+                                                panels_gateup(I), stream, nullptr, 1, 0);
 }
 
 hipError_t launch_ffn_gateup_gather(const uint16_t* x, int T, const int32_t* perm, int k,
@@ -872,20 +892,20 @@ hipError_t launch_ffn_gateup_gather(const uint16_t* x, int T, const int32_t* per
                                     hipStream_t stream) {
   if (max_rows == 0) return hipSuccess;
   if (small_batch(S, max_rows))
-    return launch_grouped<TG_SMALL, true, true>(x, offsets, S, max_rows, w13, d, 2 * I, I,
-                                                       h, I, (2 * I) / kBN, stream, perm, k, T);
+    return launch_grouped<TG_SMALL, true, true>(x, offsets, S, max_rows, w13, d, 2 * I, I, h, I,
+                                                panels_gateup(I), stream, perm, k, T);
   return launch_persistent4<true, true, false>(x, offsets, S, w13, d, 2 * I, I, h, I,
-                                               (2 * I) / kBN, stream, perm, k, T);
+                                               panels_gateup(I), stream, perm, k, T);
 }
 
 hipError_t launch_ffn_down(const uint16_t* h, const int32_t* offsets, int S, int max_rows,
                            const uint16_t* w2, int d, int I, uint16_t* y, hipStream_t stream) {
   if (max_rows == 0) return hipSuccess;
   if (small_batch(S, max_rows))
-    return launch_grouped<TG_SMALL, false, false>(h, offsets, S, max_rows, w2, I, d, 0, y,
-                                                         d, d / kBN, stream);
-  return launch_persistent4<false, false, true>(h, offsets, S, w2, I, d, 0, y, d, d / kBN, stream,
-                                                nullptr, 1, 0);
+    return launch_grouped<TG_SMALL, false, false>(h, offsets, S, max_rows, w2, I, d, 0, y, d,
+                                                  panels_down(d), stream);
+  return launch_persistent4<false, false, true>(h, offsets, S, w2, I, d, 0, y, d, panels_down(d),
+                                                stream, nullptr, 1, 0);
 }
 
 hipError_t launch_expert_ffn(const uint16_t* x_perm, const int32_t* offsets, int S, int max_rows,

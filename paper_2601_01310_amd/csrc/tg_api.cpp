@@ -45,15 +45,19 @@ tg_status check_gate_dims(int T, int E, int k) {
   return TG_OK;
 }
 
+// Hidden and intermediate sizes: multiples of 64 (the GEMMs' K stage), at
+// least 128 (two K stages).
 tg_status check_hidden(int d, const char* name) {
   if (d <= 0) return fail(TG_ERR_BAD_DIM, "%s=%d must be > 0", name, d);
-  if (d % 256) return fail(TG_ERR_UNSUPPORTED, "%s=%d is not a multiple of 256", name, d);
+  if (d % 64 || d < 128)
+    return fail(TG_ERR_UNSUPPORTED, "%s=%d is not a multiple of 64 of at least 128", name, d);
   return TG_OK;
 }
 
 tg_status check_inter(int I) {
   if (I <= 0) return fail(TG_ERR_BAD_DIM, "I=%d must be > 0", I);
-  if (I % 128) return fail(TG_ERR_UNSUPPORTED, "I=%d is not a multiple of 128", I);
+  if (I % 64 || I < 128)
+    return fail(TG_ERR_UNSUPPORTED, "I=%d is not a multiple of 64 of at least 128", I);
   return TG_OK;
 }
 

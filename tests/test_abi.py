@@ -107,7 +107,9 @@ def _ffn(lib, **kw):
 def test_expert_ffn_rejects_bad_arguments(lib):
     assert _ffn(lib, I=100) == tg.TG_ERR_UNSUPPORTED
     assert _ffn(lib, I=0) == tg.TG_ERR_BAD_DIM
-    assert _ffn(lib, d=128) == tg.TG_ERR_UNSUPPORTED
+    assert _ffn(lib, d=96) == tg.TG_ERR_UNSUPPORTED   # not a multiple of 64
+    assert _ffn(lib, d=64) == tg.TG_ERR_UNSUPPORTED   # fewer than two K stages
+    assert _ffn(lib, I=64) == tg.TG_ERR_UNSUPPORTED
     assert _ffn(lib, rows=-1) == tg.TG_ERR_BAD_DIM
     assert _ffn(lib, S=0) == tg.TG_ERR_BAD_DIM
     assert _ffn(lib, h=None) == tg.TG_ERR_NULL_ARG

@@ -286,6 +286,55 @@ def test_largest_supported_shapes_match_oracle(gate, T):
         assert np.array_equal(f["out"], g["out"]), "fused differs from stepwise"
 
 
+@pytest.mark.parametrize("d,I,T", [(320, 192, 64), (320, 192, 256), (2880, 2880, 256)],
+                         ids=["d320_I192_small", "d320_I192_persistent", "d2880_I2880_persistent"])
+def test_widths_off_the_panel_grid_match_oracle(d, I, T):
+    """d and I multiples of 64 but not of the weight panels (256 output
+    columns for the down projection, 128 gate + 128 up for gate/up): each
+    slot's last panel is partial. Routing exact, outputs within tolerance,
+    stepwise and fused calls identical, and the shadow failover run
+    bit-identical; T=64 takes the 32-row tiles, T=256 the persistent ones."""
+    print(f"[gpu] off-grid widths d={d} I={I} T={T}", flush=True)
+    wl = synth.make_custom(T=T, d=d, E=8, k=2, I=I, n_local=8, shadow_experts=[0, 5],
+                           gate="weights", seed=21, device=DEV, fail_experts=[5])
+    g = G.run_stepwise(wl)
+    r = _oracle_full(wl)
+    assert np.array_equal(g["logits"], r["logits"])
+    G.assert_routing_equal(g, r)
+    G.assert_close_bf16(g["h"], r["h"], "h")
+    G.assert_close_bf16(g["y"], r["y"], "y")
+    G.assert_close_bf16(g["out"], r["out"], "out")
+    f = G.run_fused(wl)
+    assert np.array_equal(f["out"], g["out"]), "fused differs from stepwise"
+    fo = G.run_fused(wl, wl.alive_after_failure())
+    assert np.array_equal(fo["out"], f["out"]), "failover output differs"
+
+
+def test_down_spill_with_a_partial_last_panel_matches_oracle():
+    """d = 320: the down projection has two column panels per slot, the
+    second holding 64 valid columns. 130 row blocks make 260 tiles, so 4
+    spill into 16 quarter tiles; the quarters of the second panel's right
+    half have no valid column and are skipped. Every row is checked against
+    the oracle."""
+    d, I, S = 320, 192, 10
+    counts = [3300] * 9 + [3280]  # 13 row blocks of 256 each
+    g = torch.Generator().manual_seed(23)
+    P = sum(counts)
+    x = torch.randn((P, d), generator=g).to(torch.bfloat16).to(DEV)
+    w13 = (torch.randn((S, 2 * I, d), generator=g) * 0.02).to(torch.bfloat16).to(DEV)
+    w2 = (torch.randn((S, d, I), generator=g) * 0.02).to(torch.bfloat16).to(DEV)
+    off = np.concatenate([[0], np.cumsum(counts)]).astype(np.int32)
+    h = torch.zeros((P, I), dtype=torch.bfloat16, device=DEV)
+    y = torch.full((P, d), 7, dtype=torch.int16, device=DEV).view(torch.bfloat16)
+    tg.tg_expert_ffn_grouped(x, torch.from_numpy(off).to(DEV), S, P, w13, w2, d, I, h, y)
+    torch.cuda.synchronize()
+    Y = u16(y)
+    for s in range(S):
+        hr, yr = O.expert_ffn(u16(x[off[s]:off[s + 1]]), u16(w13[s]), u16(w2[s]))
+        G.assert_close_bf16(u16(h[off[s]:off[s + 1]]), hr, f"h slot {s}")
+        G.assert_close_bf16(Y[off[s]:off[s + 1]], yr, f"y slot {s}")
+
+
 def test_empty_batch():
     wl = synth.make_custom(T=4, d=256, E=8, k=2, I=128, n_local=8, shadow_experts=[],
                            gate="weights", seed=5, device=DEV)
