@@ -25,9 +25,10 @@
  *   - Calls are reentrant; concurrent calls must not share output or
  *     workspace buffers.
  *   - Shape limits: 1 <= k <= min(E, 32), E <= 1024, 1 <= S <= 1024,
- *     1 <= R <= 16, d and I multiples of 64 and at least 128, T * k < 2^31, and one
- *     slot's weights under 2 GiB (4 * I * d < 2^31 bytes). T may be 0.
- *     Other shapes return TG_ERR_UNSUPPORTED.
+ *     1 <= R <= 16, d and I multiples of 64 and at least 128,
+ *     T * k < 2^31, and one slot's weights under 2 GiB
+ *     (4 * I * d < 2^31 bytes). T may be 0. Other shapes return
+ *     TG_ERR_UNSUPPORTED.
  */
 #ifndef TG_H_
 #define TG_H_
