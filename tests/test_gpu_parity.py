@@ -233,6 +233,8 @@ RANDOM_CASES = [
     (300, 768, 256, 8, 128, 32, [3, 4, 30], "logits", 105),
     (129, 256, 40, 32, 128, 40, [39], "logits", 106),
     (1000, 256, 4, 4, 128, 4, [2, 2], "weights", 107),   # k = E; two shadows of one expert
+    (77, 192, 16, 3, 320, 16, [4], "weights", 108),      # d, I off the panel grid
+    (700, 448, 12, 2, 192, 12, [0, 11], "weights", 109),
 ]
 
 
