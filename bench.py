@@ -581,14 +581,26 @@ def main():
     failover = None
     if not args.failover and not torch.equal(wl.alive_after_failure(), wl.alive):
         # The same inputs with the workload's failed primaries rerouted to
-        # their shadows: the rerouted run should cost the same.
-        f.set_alive(wl.alive_after_failure())
-        for _ in range(args.warmup):
-            f(stream)
-        fo_ev, fo_ms = timed_steps(args.steps)
-        failover = {"ms_per_step": fo_ms, "step_ms_p50": fo_ev[len(fo_ev) // 2],
-                    "routed_pairs": int(f.slot_offsets[-1])}
+        # their shadows: the rerouted run should cost the same. The two
+        # configurations alternate in four blocks of steps, so that both see
+        # the same clock (the GPU runs hotter after the timed loop above).
+        fail_alive, n = wl.alive_after_failure(), max(args.steps // 4, 1)
+        per = {"healthy": [], "failover": []}
+        for _ in range(2):
+            for tag, al in (("healthy", wl.alive), ("failover", fail_alive)):
+                f.set_alive(al)
+                for _ in range(max(args.warmup // 2, 1)):
+                    f(stream)
+                per[tag] += timed_steps(n)[0]
+        f.set_alive(fail_alive)
+        f(stream)
+        torch.cuda.synchronize()
+        fo_pairs = int(f.slot_offsets[-1])
         f.set_alive(wl.alive)
+        med = {t: sorted(v)[len(v) // 2] for t, v in per.items()}
+        failover = {"step_ms_p50": med["failover"], "healthy_step_ms_p50": med["healthy"],
+                    "cost": med["failover"] / med["healthy"] - 1.0, "routed_pairs": fo_pairs,
+                    "steps_each": 2 * n}
 
     d, I = wl.d, wl.I
     gemm1_flop = 4.0 * d * I * P
