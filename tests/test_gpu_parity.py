@@ -337,6 +337,47 @@ def test_down_spill_with_a_partial_last_panel_matches_oracle():
         G.assert_close_bf16(Y[off[s]:off[s + 1]], yr, f"y slot {s}")
 
 
+def _sweep_cases(seed, n):
+    rng = np.random.default_rng(seed)
+    out = []
+    for _ in range(n):
+        E = int(rng.integers(1, 65))
+        k = int(rng.integers(1, min(E, 8) + 1))
+        n_local = int(rng.integers(1, E + 1))
+        T = int(rng.choice([1, 2, 7, 33, 64, 129, 300, 600, 1500]))
+        d, I = int(rng.integers(2, 17)) * 64, int(rng.integers(2, 13)) * 64
+        shadows = sorted(rng.choice(n_local, size=min(int(rng.integers(0, 4)), n_local)).tolist())
+        gate = "weights" if rng.random() < 0.5 else "logits"
+        out.append((T, d, E, k, I, n_local, shadows, gate, int(rng.integers(1 << 30)),
+                    float(rng.random())))
+    return out
+
+
+@pytest.mark.parametrize("case", _sweep_cases(11, 24), ids=lambda c: f"T{c[0]}_d{c[1]}_E{c[2]}_k{c[3]}_I{c[4]}")
+def test_seeded_random_sweep_matches_oracle(case):
+    """A seeded sweep over T, d, I (multiples of 64), E, k, local experts,
+    shadows and gating mode, each run healthy and with a random set of dead
+    slots: routing exact, outputs within tolerance, fused equal to stepwise."""
+    T, d, E, k, I, n_local, shadows, gate, seed, p_fail = case
+    print(f"[gpu] sweep case {case}", flush=True)
+    wl = synth.make_custom(T=T, d=d, E=E, k=k, I=I, n_local=n_local, shadow_experts=shadows,
+                           gate=gate, seed=seed, device=DEV)
+    rng = np.random.default_rng(seed)
+    alive = wl.alive.clone()
+    if wl.S > 1 and p_fail < 0.7:
+        dead = rng.choice(wl.S, size=int(rng.integers(1, wl.S)), replace=False)
+        alive[torch.from_numpy(dead).to(DEV)] = 0
+    for al in (wl.alive, alive):
+        g = G.run_stepwise(wl, al)
+        r = _oracle_full(wl, al)
+        if g["logits"] is not None:
+            assert np.array_equal(g["logits"], r["logits"])
+        G.assert_routing_equal(g, r)
+        G.assert_close_bf16(g["out"], r["out"], "out")
+        f = G.run_fused(wl, al)
+        assert np.array_equal(f["out"], g["out"]), "fused differs from stepwise"
+
+
 def test_empty_batch():
     wl = synth.make_custom(T=4, d=256, E=8, k=2, I=128, n_local=8, shadow_experts=[],
                            gate="weights", seed=5, device=DEV)
