@@ -17,8 +17,9 @@
 //      the slot index gives every lane the lanes that share its slot, so the
 //      rank costs the same for any mix of slots, and rows follow
 //      (slot, token, rank).
-// Up to 2048 pairs, one block runs all three passes (the batch of a decode
-// step fits, and two launches are saved).
+// Up to 4096 pairs, one block runs all three passes (the batch of a decode
+// step fits, and two launches are saved; past that the three grids are
+// faster, as each group of 1024 pairs costs the one block about 1.7 us).
 // The gather then copies one activation row per routed pair with 16-byte
 // loads and stores (rows are contiguous in source and destination, so the
 // copy is fully coalesced without staging).
@@ -30,6 +31,32 @@ namespace {
 
 constexpr int kMaxS = 1024;
 constexpr int kBlock = 256;
+
+// Slot of a pair of expert e: the first live ERT candidate of e.
+// REPLAY: -1 also when the first pass's slot pr is still alive (its result
+// stands). *unserved: the expert lists a local candidate, none alive.
+template <bool REPLAY>
+__device__ __forceinline__ int resolve_expert(int e, int pr, const int32_t* __restrict__ ert,
+                                              int E, int R, const uint8_t* __restrict__ alive,
+                                              int S, bool* unserved) {
+  int slot = -1;
+  bool listed = false;
+  if (e >= 0 && e < E) {
+    for (int r = 0; r < R; ++r) {
+      const int c = ert[(size_t)e * R + r];
+      if (c >= 0 && c < S) {
+        listed = true;
+        if (alive[c]) {
+          slot = c;
+          break;
+        }
+      }
+    }
+  }
+  *unserved = slot < 0 && listed;
+  if (REPLAY && pr >= 0 && pr < S && alive[pr]) slot = -1;  // first-pass result stands
+  return slot;
+}
 
 // Slot that pair p is computed on: the first live ERT candidate of its
 // expert; -2 for a token outside the batch. REPLAY: -1 also when the first
@@ -50,24 +77,21 @@ __device__ __forceinline__ int resolve_pair(int p, const int32_t* __restrict__ i
   } else if (token_valid && !token_valid[p / k]) {
     return -2;
   }
-  const int e = ids[p];
-  int slot = -1;
-  bool listed = false;
-  if (e >= 0 && e < E) {
-    for (int r = 0; r < R; ++r) {
-      const int c = ert[(size_t)e * R + r];
-      if (c >= 0 && c < S) {
-        listed = true;
-        if (alive[c]) {
-          slot = c;
-          break;
-        }
-      }
-    }
+  return resolve_expert<REPLAY>(ids[p], pr, ert, E, R, alive, S, unserved);
+}
+
+// Lanes of the wave that hold a routed pair (s >= 0) on the same slot as
+// this lane: start from the routed lanes and keep, for every bit of the slot
+// index (sbits bits), the lanes that agree with this lane on that bit. The
+// cost is the same for any mix of slots. 0 on lanes with s < 0.
+__device__ __forceinline__ uint64_t same_slot_lanes(int s, int sbits) {
+  uint64_t eq = __ballot(s >= 0);
+  for (int b = 0; b < sbits; ++b) {
+    const bool bit = (s >> b) & 1;
+    const uint64_t mb = __ballot(bit);
+    eq &= bit ? mb : ~mb;
   }
-  *unserved = slot < 0 && listed;
-  if (REPLAY && pr >= 0 && pr < S && alive[pr]) slot = -1;  // first-pass result stands
-  return slot;
+  return s >= 0 ? eq : 0;
 }
 
 // REPLAY: `prior` holds the first pass's slot of every pair; out_slot gets
@@ -211,16 +235,8 @@ __global__ __launch_bounds__(kBlock) void scatter_kernel(const int32_t* __restri
       s = pair_slot[p];
       if (s < 0) pair_row[p] = -1;
     }
-    // Lanes holding a routed pair whose slot equals this lane's: start from
-    // the routed lanes and keep, for every bit of the slot index, the lanes
-    // that agree with this lane on that bit.
-    uint64_t eq = __ballot(s >= 0);
-    if (!eq) continue;  // uniform
-    for (int b = 0; b < sbits; ++b) {
-      const bool bit = (s >> b) & 1;
-      const uint64_t mb = __ballot(bit);
-      eq &= bit ? mb : ~mb;
-    }
+    if (!__ballot(s >= 0)) continue;  // uniform
+    const uint64_t eq = same_slot_lanes(s, sbits);
     if (s >= 0) {
       const int row = cnt[wave][s] + __builtin_popcountll(eq & lt);
       perm[row] = p;
@@ -233,102 +249,158 @@ __global__ __launch_bounds__(kBlock) void scatter_kernel(const int32_t* __restri
 }
 
 // All three passes in one block of 1024 threads, for at most kSmallPairs
-// pairs: thread i resolves pairs i, i + 1024, ...; a block-wide scan gives
-// the offsets; then the pairs are ranked 1024 at a time in pair order (wave
-// w holds pairs 64w .. 64w+63 of the group) exactly as scatter_kernel does,
-// so rows follow (slot, token, rank).
+// pairs; thread i takes pairs i, i + 1024, ... The ERT and the liveness mask
+// are first copied to LDS while the pairs' expert ids load, so resolving a
+// pair costs one memory latency. Each wave counts its pairs per slot with
+// same_slot_lanes (one LDS add per distinct slot), a wave scan with one
+// barrier gives the slot offsets, and the pairs are then ranked 1024 at a
+// time in pair order (wave w holds pairs 64w .. 64w+63 of the group) exactly
+// as scatter_kernel does, so rows follow (slot, token, rank).
 constexpr int kOneBlock = 1024;
-constexpr int kSmallPairs = 2048;
+constexpr int kSmallPairs = 4096;
 constexpr int kSmallPer = kSmallPairs / kOneBlock;
+constexpr int kMaxErt = 1024 * 16;  // E * R entries staged in LDS (E <= 1024, R <= 16)
 
 template <bool REPLAY>
 __global__ __launch_bounds__(kOneBlock) void dispatch_one_block_kernel(
     const int32_t* __restrict__ ids, int npairs, int k, const int32_t* __restrict__ ert, int E,
-    int R, const uint8_t* __restrict__ alive, int S, const uint8_t* __restrict__ token_valid,
-    const int32_t* __restrict__ prior, int32_t* __restrict__ out_slot, int32_t* __restrict__ counts,
-    int32_t* __restrict__ offsets, int32_t* __restrict__ perm, int32_t* __restrict__ pair_row,
-    int32_t* __restrict__ n_unserved, int32_t* __restrict__ total_out) {
+    int R, const uint8_t* __restrict__ alive, int S, int sbits,
+    const uint8_t* __restrict__ token_valid, const int32_t* __restrict__ prior,
+    int32_t* __restrict__ out_slot, int32_t* __restrict__ counts, int32_t* __restrict__ offsets,
+    int32_t* __restrict__ perm, int32_t* __restrict__ pair_row, int32_t* __restrict__ n_unserved,
+    int32_t* __restrict__ total_out) {
   constexpr int kWaves = kOneBlock / kWave;
+  // cnt[w][s]: pairs of wave w on slot s in the current group of 1024, then
+  // their first row; 0 wherever wave w has no pair on s.
   __shared__ int cnt[kWaves][kMaxS];
   __shared__ int run[kMaxS];
-  __shared__ int sc[2][kOneBlock];
+  __shared__ int ert_s[kMaxErt];
+  __shared__ uint8_t alive_s[kMaxS];
+  __shared__ int wsum[kWaves];
   __shared__ int nu;
   const int tid = threadIdx.x;
   const int wave = tid / kWave, lane = lane_id();
-  for (int s = tid; s < S; s += kOneBlock) run[s] = 0;
-  if (tid == 0) nu = 0;
-  __syncthreads();
-  int my_slot[kSmallPer];
+  const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+
+  // Loads that do not depend on one another: the pairs' ids (and first-pass
+  // slots or batch flags), the ERT and the mask. Raw values only, so no load
+  // waits for another.
+  // Every lane loads (indices past the end read the last pair, and their
+  // values are never used), so no load sits in a divergent branch.
+  int e_of[kSmallPer], f_of[kSmallPer];
+  if (npairs > 0) {
 #pragma unroll
-  for (int i = 0; i < kSmallPer; ++i) {
-    const int p = tid + i * kOneBlock;
-    my_slot[i] = -1;
-    if (p < npairs) {
-      bool unserved;
-      my_slot[i] =
-          resolve_pair<REPLAY>(p, ids, k, ert, E, R, alive, S, token_valid, prior, &unserved);
-      out_slot[p] = my_slot[i];
-      if (unserved) atomicAdd(&nu, 1);
-      if (my_slot[i] >= 0) atomicAdd(&run[my_slot[i]], 1);
+    for (int i = 0; i < kSmallPer; ++i) {
+      const int p = min(tid + i * kOneBlock, npairs - 1);
+      e_of[i] = ids[p];
+      f_of[i] = REPLAY ? prior[p] : 1;
+    }
+    if (!REPLAY && token_valid) {
+#pragma unroll
+      for (int i = 0; i < kSmallPer; ++i)
+        f_of[i] = token_valid[min(tid + i * kOneBlock, npairs - 1) / k];
     }
   }
-  __syncthreads();
-  // Exclusive scan of the slot totals (Hillis-Steele over 1024 entries).
-  const int total = (tid < S) ? run[tid] : 0;
-  sc[0][tid] = total;
-  __syncthreads();
-  int cur = 0;
-  for (int off = 1; off < kOneBlock; off <<= 1) {
-    sc[cur ^ 1][tid] = sc[cur][tid] + (tid >= off ? sc[cur][tid - off] : 0);
-    cur ^= 1;
-    __syncthreads();
+  for (int j = tid; j < E * R; j += kOneBlock) ert_s[j] = ert[j];
+  for (int j = tid; j < S; j += kOneBlock) {
+    alive_s[j] = alive[j];
+    run[j] = 0;
   }
-  const int incl = sc[cur][tid];
+  for (int j = tid; j < kWaves * S; j += kOneBlock) cnt[j / S][j % S] = 0;
+  if (tid == 0) nu = 0;
+  __syncthreads();
+
+  // Global stores wait until the end: on this chip a wait for a load also
+  // waits for every earlier store, so stores issued here would stall the
+  // passes below.
+  int my_slot[kSmallPer];
+  uint64_t my_eq[kSmallPer];
+#pragma unroll
+  for (int i = 0; i < kSmallPer; ++i) {
+    my_slot[i] = -1;
+    my_eq[i] = 0;
+    if (i * kOneBlock >= npairs) continue;  // uniform
+    const int p = tid + i * kOneBlock;
+    bool unserved = false;
+    int s = -1;
+    if (p < npairs) {
+      if (REPLAY ? f_of[i] != -2 : f_of[i] != 0)
+        s = resolve_expert<REPLAY>(e_of[i], REPLAY ? f_of[i] : 0, ert_s, E, R, alive_s, S,
+                                   &unserved);
+      else
+        s = REPLAY ? -1 : -2;
+    }
+    const int n_un = __builtin_popcountll(__ballot(unserved));
+    if (lane == 0 && n_un) atomicAdd(&nu, n_un);
+    const uint64_t eq = same_slot_lanes(s, sbits);
+    if (s >= 0 && !(eq & lt)) atomicAdd(&run[s], __builtin_popcountll(eq));
+    my_slot[i] = s;
+    my_eq[i] = eq;
+  }
+  __syncthreads();
+
+  // Exclusive scan of the slot totals: a wave scan per 64 slots, then the
+  // totals of the waves before.
+  const int total = (tid < S) ? run[tid] : 0;
+  int incl = total;
+#pragma unroll
+  for (int off = 1; off < kWave; off <<= 1) {
+    const int t = __shfl_up(incl, off);
+    if (lane >= off) incl += t;
+  }
+  if (lane == kWave - 1) wsum[wave] = incl;
+  __syncthreads();
+  for (int w = 0; w < wave; ++w) incl += wsum[w];
+  if (tid < S) run[tid] = incl - total;  // next row of the slot
+
+  int my_row[kSmallPer];
+#pragma unroll
+  for (int i = 0; i < kSmallPer; ++i) my_row[i] = -1;
+#pragma unroll
+  for (int i = 0; i < kSmallPer; ++i) {
+    if (i * kOneBlock >= npairs) break;  // uniform
+    const int s = my_slot[i];
+    const uint64_t eq = my_eq[i];
+    const bool lead = s >= 0 && !(eq & lt);
+    if (lead) cnt[wave][s] = __builtin_popcountll(eq);
+    __syncthreads();
+    // Thread q turns slot q's per-wave counts into first rows (all reads
+    // first, so they are in flight together; absent waves keep 0).
+    if (tid < S) {
+      int v[kWaves];
+#pragma unroll
+      for (int w = 0; w < kWaves; ++w) v[w] = cnt[w][tid];
+      int r = run[tid];
+#pragma unroll
+      for (int w = 0; w < kWaves; ++w) {
+        cnt[w][tid] = v[w] ? r : 0;
+        r += v[w];
+      }
+      run[tid] = r;
+    }
+    __syncthreads();
+    if (s >= 0) my_row[i] = cnt[wave][s] + __builtin_popcountll(eq & lt);
+    // Every lane's read above precedes this write in the wave's LDS order.
+    if (lead) cnt[wave][s] = 0;
+  }
+
   if (tid < S) {
     counts[tid] = total;
     offsets[tid] = incl - total;
-    run[tid] = incl - total;
   }
   if (tid == S - 1) {
     offsets[S] = incl;
     if (total_out) total_out[0] = incl;
   }
   if (tid == 0) n_unserved[0] = nu;
-  const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
 #pragma unroll
   for (int i = 0; i < kSmallPer; ++i) {
-    if (i * kOneBlock >= npairs) break;  // uniform
-    for (int j = tid; j < kWaves * S; j += kOneBlock) cnt[j / S][j % S] = 0;
-    __syncthreads();
-    const int s = my_slot[i];
-    if (s >= 0) atomicAdd(&cnt[wave][s], 1);
-    __syncthreads();
-    for (int q = tid; q < S; q += kOneBlock) {
-      int r = run[q];
-      for (int w = 0; w < kWaves; ++w) {
-        const int v = cnt[w][q];
-        cnt[w][q] = r;
-        r += v;
-      }
-      run[q] = r;
-    }
-    __syncthreads();
     const int p = tid + i * kOneBlock;
-    if (p < npairs && s < 0) pair_row[p] = -1;
-    uint64_t active = __ballot(s >= 0);
-    while (active) {
-      const int leader = __builtin_ctzll(active);
-      const int sl = __shfl(s, leader);
-      const uint64_t m = __ballot(s == sl) & active;
-      if (s == sl) {
-        const int row = cnt[wave][sl] + __builtin_popcountll(m & lt);
-        perm[row] = p;
-        pair_row[p] = row;
-      }
-      if (lane == leader) cnt[wave][sl] += __builtin_popcountll(m);
-      active &= ~m;
+    if (p < npairs) {
+      out_slot[p] = my_slot[i];
+      pair_row[p] = my_row[i];
+      if (my_row[i] >= 0) perm[my_row[i]] = p;
     }
-    __syncthreads();
   }
 }
 
@@ -376,15 +448,16 @@ hipError_t remap_dispatch(bool replay, const int32_t* ids, int T, int k, const i
   const size_t hist_bytes = ((size_t)nchunks * S * sizeof(int32_t) + 255) & ~(size_t)255;
   int32_t* hist = static_cast<int32_t*>(ws);
   int32_t* unserved_chunk = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + hist_bytes);
+  const int sbits = (S > 1) ? 32 - __builtin_clz((unsigned)(S - 1)) : 0;
   if (npairs <= kSmallPairs) {
     if (replay)
       hipLaunchKernelGGL(dispatch_one_block_kernel<true>, dim3(1), dim3(kOneBlock), 0, stream, ids,
-                         npairs, k, ert, E, R, alive, S, nullptr, prior, pair_slot, counts,
+                         npairs, k, ert, E, R, alive, S, sbits, nullptr, prior, pair_slot, counts,
                          offsets, perm, pair_row, n_unserved, total_out);
     else
       hipLaunchKernelGGL(dispatch_one_block_kernel<false>, dim3(1), dim3(kOneBlock), 0, stream,
-                         ids, npairs, k, ert, E, R, alive, S, token_valid, nullptr, pair_slot,
-                         counts, offsets, perm, pair_row, n_unserved, total_out);
+                         ids, npairs, k, ert, E, R, alive, S, sbits, token_valid, nullptr,
+                         pair_slot, counts, offsets, perm, pair_row, n_unserved, total_out);
     if (x_perm && npairs > 0) {
       const int nch = d / 8;
       const long maxq = (long)npairs * nch;
@@ -409,7 +482,6 @@ hipError_t remap_dispatch(bool replay, const int32_t* ids, int T, int k, const i
   hipLaunchKernelGGL(scan_kernel, dim3(1), dim3(1024), 0, stream, hist, unserved_chunk, nchunks, S,
                      counts, offsets, n_unserved, total_out);
   if (nchunks > 0) {
-    const int sbits = (S > 1) ? 32 - __builtin_clz((unsigned)(S - 1)) : 0;
     hipLaunchKernelGGL(scatter_kernel, dim3(nchunks), dim3(kBlock), 0, stream, pair_slot, npairs, S,
                        nchunks, sbits, hist, offsets, perm, pair_row, chunk);
     if (x_perm) {

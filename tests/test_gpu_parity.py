@@ -233,8 +233,10 @@ RANDOM_CASES = [
     (300, 768, 256, 8, 128, 32, [3, 4, 30], "logits", 105),
     (129, 256, 40, 32, 128, 40, [39], "logits", 106),
     (1000, 256, 4, 4, 128, 4, [2, 2], "weights", 107),   # k = E; two shadows of one expert
+    (1024, 256, 16, 4, 128, 12, [3], "weights", 111),    # 4096 pairs: the one-block dispatch's limit
     (77, 192, 16, 3, 320, 16, [4], "weights", 108),      # d, I off the panel grid
     (700, 448, 12, 2, 192, 12, [0, 11], "weights", 109),
+    (2731, 256, 24, 3, 128, 20, [2, 9], "logits", 110),  # 8193 pairs: ragged last dispatch chunk
 ]
 
 
