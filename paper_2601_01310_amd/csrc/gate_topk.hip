@@ -6,7 +6,9 @@
 // lane the full sums, and the float64 sum is rounded once to float32.
 // When the gate matrix fits (E*d*2 <= 96 KB) a block of 16 waves (16
 // tokens) stages it in LDS once, so the matrix is read from memory once per
-// 16 tokens instead of once per token. Top-k runs as k rounds of a wave
+// 16 tokens instead of once per token; up to E*d*4 = 128 KB it is staged
+// widened to float32, which takes the unpacking out of the dot product (the
+// loop is bound by the vector ALU). Top-k runs as k rounds of a wave
 // arg-max over the float32 logits (larger first, ties to the lower expert
 // id), the cross-lane step in DPP row operations and lane reads; lane j
 // keeps the j-th winner, the k exponentials are formed in parallel and
@@ -20,6 +22,8 @@ namespace {
 constexpr int kWaves = 4;          // waves per block (unstaged kernels)
 constexpr int kStagedWaves = 16;   // waves (= tokens) per block when the gate matrix is staged
 constexpr int kStageElems = 48 * 1024;  // 96 KB of bf16
+constexpr int kStageElemsF32 = 32 * 1024;  // 128 KB of float32
+constexpr int kStageBytes = 128 * 1024;
 constexpr int kStagedMaxE = kStageElems / 256;  // staged only when E * d fits, d >= 256
 
 __device__ __forceinline__ bool better(float v, int id, float bv, int bid) {
@@ -181,32 +185,82 @@ __device__ __forceinline__ void logits8(const uint4* __restrict__ xr, WgPtr wg, 
   }
 }
 
-// Weight mode, one token per wave. STAGED: a block of 16 waves first
-// copies the gate matrix to LDS; otherwise 4 waves read it from global
-// memory.
-template <bool STAGED>
-__global__ __launch_bounds__(STAGED ? 64 * kStagedWaves : 64 * kWaves) void gate_weights_topk_kernel(
+// The same against a gate matrix staged in LDS as float32 (two float4 per
+// chunk of 8), which saves the unpacking of every weight; the products and
+// their order are those of logits8.
+__device__ __forceinline__ void logits8_f32(const uint4* __restrict__ xr, const float* wg, int d,
+                                            int E, int e0, float* lg) {
+  const int lane = lane_id();
+  const int nchunk = d / 8;
+  double acc[8];
+#pragma unroll
+  for (int q = 0; q < 8; ++q) acc[q] = 0.0;
+  for (int c = lane; c < nchunk; c += kWave) {
+    const uint4 xv = xr[c];
+    const uint32_t xs[4] = {xv.x, xv.y, xv.z, xv.w};
+    double xd[8];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      xd[2 * i] = (double)__uint_as_float(xs[i] << 16);
+      xd[2 * i + 1] = (double)__uint_as_float(xs[i] & 0xffff0000u);
+    }
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const int e = e0 + q;
+      if (e < E) {
+        const float4* wr = reinterpret_cast<const float4*>(wg + (size_t)e * d) + 2 * c;
+        const float4 w0 = wr[0], w1 = wr[1];
+        const float wf[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
+#pragma unroll
+        for (int i = 0; i < 8; ++i) acc[q] = fma(xd[i], (double)wf[i], acc[q]);
+      }
+    }
+  }
+#pragma unroll
+  for (int q = 0; q < 8; ++q) {
+    const double sum = wave_sum_f64(acc[q]);
+    if (lane == 0 && e0 + q < E) lg[e0 + q] = (float)sum;
+  }
+}
+
+// Weight mode, one token per wave. STAGE 0: 4 waves read the gate matrix
+// from global memory; otherwise a block of 16 waves first copies it to LDS,
+// as bf16 (STAGE 1) or, when it fits in 128 KB that way, widened to float32
+// (STAGE 2).
+template <int STAGE>
+__global__ __launch_bounds__(STAGE ? 64 * kStagedWaves : 64 * kWaves) void gate_weights_topk_kernel(
     const uint16_t* __restrict__ x, const uint16_t* __restrict__ wg, int T, int d, int E, int k,
     float* __restrict__ logits_out, int32_t* __restrict__ ids, float* __restrict__ w) {
-  constexpr int NW = STAGED ? kStagedWaves : kWaves;
-  constexpr int LG = STAGED ? kStagedMaxE : 1024;
-  __shared__ __attribute__((aligned(16))) uint16_t wg_s[STAGED ? kStageElems : 8];
+  constexpr int NW = STAGE ? kStagedWaves : kWaves;
+  constexpr int LG = STAGE ? kStagedMaxE : 1024;
+  __shared__ __attribute__((aligned(16))) uint32_t wg_s[STAGE ? kStageBytes / 4 : 4];
   __shared__ float lg_s[NW][LG];
   const int wave = threadIdx.x / kWave;
   const int lane = lane_id();
   float* lg = lg_s[wave];
-  if (STAGED) {
+  if (STAGE) {
     const int n16 = E * d / 8;
-    for (int i = threadIdx.x; i < n16; i += 64 * NW)
-      reinterpret_cast<uint4*>(wg_s)[i] = reinterpret_cast<const uint4*>(wg)[i];
+    for (int i = threadIdx.x; i < n16; i += 64 * NW) {
+      const uint4 v = reinterpret_cast<const uint4*>(wg)[i];
+      if (STAGE == 1) {
+        reinterpret_cast<uint4*>(wg_s)[i] = v;
+      } else {
+        const uint32_t m = 0xffff0000u;
+        reinterpret_cast<uint4*>(wg_s)[2 * i] = make_uint4(v.x << 16, v.x & m, v.y << 16, v.y & m);
+        reinterpret_cast<uint4*>(wg_s)[2 * i + 1] =
+            make_uint4(v.z << 16, v.z & m, v.w << 16, v.w & m);
+      }
+    }
     __syncthreads();
   }
   const int t = blockIdx.x * NW + wave;
   if (t < T) {
     const uint4* xr = reinterpret_cast<const uint4*>(x + (size_t)t * d);
     for (int e0 = 0; e0 < E; e0 += 8) {
-      if (STAGED)
-        logits8(xr, static_cast<const uint16_t*>(wg_s), d, E, e0, lg);
+      if (STAGE == 2)
+        logits8_f32(xr, reinterpret_cast<const float*>(wg_s), d, E, e0, lg);
+      else if (STAGE == 1)
+        logits8(xr, reinterpret_cast<const uint16_t*>(wg_s), d, E, e0, lg);
       else
         logits8(xr, wg, d, E, e0, lg);
     }
@@ -335,11 +389,14 @@ hipError_t launch_gate_topk(const uint16_t* x, const uint16_t* wg, const float* 
   } else if (logits_in) {
     hipLaunchKernelGGL(logits_topk_kernel, dim3((T + kWaves - 1) / kWaves), dim3(256), 0, stream,
                        logits_in, T, E, k, ids, w);
+  } else if ((long)E * d <= kStageElemsF32 && E <= kStagedMaxE) {
+    hipLaunchKernelGGL(gate_weights_topk_kernel<2>, dim3((T + kStagedWaves - 1) / kStagedWaves),
+                       dim3(64 * kStagedWaves), 0, stream, x, wg, T, d, E, k, logits_out, ids, w);
   } else if ((long)E * d <= kStageElems && E <= kStagedMaxE) {
-    hipLaunchKernelGGL(gate_weights_topk_kernel<true>, dim3((T + kStagedWaves - 1) / kStagedWaves),
+    hipLaunchKernelGGL(gate_weights_topk_kernel<1>, dim3((T + kStagedWaves - 1) / kStagedWaves),
                        dim3(64 * kStagedWaves), 0, stream, x, wg, T, d, E, k, logits_out, ids, w);
   } else {
-    hipLaunchKernelGGL(gate_weights_topk_kernel<false>, dim3((T + kWaves - 1) / kWaves), dim3(256),
+    hipLaunchKernelGGL(gate_weights_topk_kernel<0>, dim3((T + kWaves - 1) / kWaves), dim3(256),
                        0, stream, x, wg, T, d, E, k, logits_out, ids, w);
   }
   return hipGetLastError();

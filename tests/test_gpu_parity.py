@@ -237,6 +237,8 @@ RANDOM_CASES = [
     (77, 192, 16, 3, 320, 16, [4], "weights", 108),      # d, I off the panel grid
     (700, 448, 12, 2, 192, 12, [0, 11], "weights", 109),
     (2731, 256, 24, 3, 128, 20, [2, 9], "logits", 110),  # 8193 pairs: ragged last dispatch chunk
+    (150, 2048, 20, 2, 128, 16, [1], "weights", 112),    # gate matrix staged as bf16 (80 KB)
+    (150, 1024, 32, 2, 128, 16, [1], "weights", 113),    # gate matrix staged as float32 (128 KB)
 ]
 
 
