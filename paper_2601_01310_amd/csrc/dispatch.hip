@@ -11,7 +11,9 @@
 //      otherwise given its first live candidate now, to be recomputed;
 //   2. scan: per-slot totals, exclusive slot offsets, and the position of
 //      every (chunk, slot) within its slot in chunk order (the histograms
-//      are slot-major, so one wave scans one slot's chunks);
+//      are slot-major, so one wave scans one slot's chunks). When S times
+//      the number of chunks is at most 16384, each scatter block does this
+//      for itself from the whole histogram instead, and the launch is saved;
 //   3. scatter: each wave walks an equal share of a chunk in pair order and
 //      ranks the pairs of each group of 64 by slot: one ballot per bit of
 //      the slot index gives every lane the lanes that share its slot, so the
@@ -31,6 +33,7 @@ namespace {
 
 constexpr int kMaxS = 1024;
 constexpr int kBlock = 256;
+constexpr long kFusedScanHist = 16384;  // S * nchunks up to which scatter scans by itself
 
 // Slot of a pair of expert e: the first live ERT candidate of e.
 // REPLAY: -1 also when the first pass's slot pr is still alive (its result
@@ -192,15 +195,26 @@ __global__ __launch_bounds__(1024) void scan_kernel(int32_t* __restrict__ hist,
   if (tid == 0) n_unserved[0] = nu;
 }
 
-// rel[s * nchunks + c]: position of chunk c's first pair within slot s
-// (from scan_kernel); sbits: bits of the largest slot index.
-__global__ __launch_bounds__(kBlock) void scatter_kernel(const int32_t* __restrict__ pair_slot,
-                                                         int npairs, int S, int nchunks, int sbits,
-                                                         const int32_t* __restrict__ rel,
-                                                         const int32_t* __restrict__ offsets,
-                                                         int32_t* __restrict__ perm,
-                                                         int32_t* __restrict__ pair_row,
-                                                         int chunk) {
+__device__ __forceinline__ int wave_sum_int(int v) {
+#pragma unroll
+  for (int off = kWave / 2; off > 0; off >>= 1) v += __shfl_xor(v, off);
+  return v;
+}
+
+// SCAN false: hist[s * nchunks + c] is the position of chunk c's first pair
+// within slot s and offsets the slot offsets (both from scan_kernel).
+// SCAN true: hist holds the per-chunk counts of remap_count, and every block
+// derives what it needs itself (its chunk's position in each slot and the
+// slot offsets, from all of hist; for small S * nchunks this is cheaper
+// than a launch); block 0 also writes counts, offsets, the unserved count
+// and the total. sbits: bits of the largest slot index.
+template <bool SCAN>
+__global__ __launch_bounds__(kBlock) void scatter_kernel(
+    const int32_t* __restrict__ pair_slot, int npairs, int S, int nchunks, int sbits,
+    const int32_t* __restrict__ hist, const int32_t* __restrict__ unserved_chunk,
+    int32_t* __restrict__ counts, int32_t* __restrict__ offsets,
+    int32_t* __restrict__ n_unserved, int32_t* __restrict__ total_out,
+    int32_t* __restrict__ perm, int32_t* __restrict__ pair_row, int chunk) {
   constexpr int kWaves = kBlock / kWave;
   __shared__ int cnt[kWaves][kMaxS];
   const int wave = threadIdx.x / kWave;
@@ -211,15 +225,80 @@ __global__ __launch_bounds__(kBlock) void scatter_kernel(const int32_t* __restri
   const int span = ((n_c + kWaves * kWave - 1) / (kWaves * kWave)) * kWave;
   const int p0 = c0 + wave * span;
   const int p1 = min(c0 + n_c, p0 + span);
+  __shared__ int base[SCAN ? kMaxS : 1];  // first row of this chunk's pairs on each slot
+  __shared__ int tot[SCAN ? kMaxS : 1];
+  __shared__ int wsum[kWaves];
   for (int i = threadIdx.x; i < kWaves * kMaxS; i += kBlock) (&cnt[0][0])[i] = 0;
+  if (SCAN) {
+    // Wave w takes slots w, w + 4, ...; lane l the chunks l, l + 64, ...
+    for (int s = wave; s < S; s += kWaves) {
+      const int32_t* hs = hist + (size_t)s * nchunks;
+      int all = 0, before = 0;
+      for (int c = lane; c < nchunks; c += kWave) {
+        const int v = hs[c];
+        all += v;
+        if (c < (int)blockIdx.x) before += v;
+      }
+      all = wave_sum_int(all);
+      before = wave_sum_int(before);
+      if (lane == 0) {
+        tot[s] = all;
+        base[s] = before;
+      }
+    }
+  }
   __syncthreads();
+  if (SCAN) {
+    // Exclusive scan of the slot totals: thread i holds slots 4i .. 4i+3.
+    int v[4], sum = 0;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int s = 4 * threadIdx.x + j;
+      v[j] = s < S ? tot[s] : 0;
+      sum += v[j];
+    }
+    int incl = sum;
+#pragma unroll
+    for (int off = 1; off < kWave; off <<= 1) {
+      const int t = __shfl_up(incl, off);
+      if (lane >= off) incl += t;
+    }
+    if (lane == kWave - 1) wsum[wave] = incl;
+    __syncthreads();
+    for (int w = 0; w < wave; ++w) incl += wsum[w];
+    int run = incl - sum;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int s = 4 * threadIdx.x + j;
+      if (s < S) {
+        base[s] += run;
+        if (blockIdx.x == 0) {
+          counts[s] = v[j];
+          offsets[s] = run;
+        }
+      }
+      run += v[j];
+    }
+    if (blockIdx.x == 0) {
+      if (threadIdx.x == kBlock - 1) {
+        offsets[S] = run;  // the last thread's run is the grand total
+        if (total_out) total_out[0] = run;
+      }
+      if (wave == 0) {
+        int nu = 0;
+        for (int c = lane; c < nchunks; c += kWave) nu += unserved_chunk[c];
+        nu = wave_sum_int(nu);
+        if (lane == 0) n_unserved[0] = nu;
+      }
+    }
+  }
   for (int p = p0 + lane; p < p1; p += kWave) {
     const int s = pair_slot[p];
     if (s >= 0) atomicAdd(&cnt[wave][s], 1);
   }
   __syncthreads();
   for (int s = threadIdx.x; s < S; s += kBlock) {
-    int run = offsets[s] + rel[(size_t)s * nchunks + blockIdx.x];
+    int run = SCAN ? base[s] : offsets[s] + hist[(size_t)s * nchunks + blockIdx.x];
     for (int w = 0; w < kWaves; ++w) {
       const int v = cnt[w][s];
       cnt[w][s] = run;
@@ -479,11 +558,20 @@ hipError_t remap_dispatch(bool replay, const int32_t* ids, int T, int k, const i
                          npairs, k, ert, E, R, alive, S, token_valid, nullptr, pair_slot, hist,
                          unserved_chunk, chunk);
   }
-  hipLaunchKernelGGL(scan_kernel, dim3(1), dim3(1024), 0, stream, hist, unserved_chunk, nchunks, S,
-                     counts, offsets, n_unserved, total_out);
+  // A small histogram is scanned by every scatter block (one launch less).
+  const bool fused_scan = nchunks > 0 && (long)S * nchunks <= kFusedScanHist;
+  if (!fused_scan)
+    hipLaunchKernelGGL(scan_kernel, dim3(1), dim3(1024), 0, stream, hist, unserved_chunk, nchunks,
+                       S, counts, offsets, n_unserved, total_out);
   if (nchunks > 0) {
-    hipLaunchKernelGGL(scatter_kernel, dim3(nchunks), dim3(kBlock), 0, stream, pair_slot, npairs, S,
-                       nchunks, sbits, hist, offsets, perm, pair_row, chunk);
+    if (fused_scan)
+      hipLaunchKernelGGL(scatter_kernel<true>, dim3(nchunks), dim3(kBlock), 0, stream, pair_slot,
+                         npairs, S, nchunks, sbits, hist, unserved_chunk, counts, offsets,
+                         n_unserved, total_out, perm, pair_row, chunk);
+    else
+      hipLaunchKernelGGL(scatter_kernel<false>, dim3(nchunks), dim3(kBlock), 0, stream, pair_slot,
+                         npairs, S, nchunks, sbits, hist, unserved_chunk, counts, offsets,
+                         n_unserved, total_out, perm, pair_row, chunk);
     if (x_perm) {
       const int nch = d / 8;
       const long maxq = (long)npairs * nch;

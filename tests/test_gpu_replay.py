@@ -138,6 +138,7 @@ REPLAY_CASES = [
     (300, 768, 256, 8, 128, 32, [3, 4, 30], "logits", 205),
     (1000, 256, 4, 4, 128, 4, [2, 2], "weights", 207),
     (1024, 256, 32, 4, 128, 24, [0, 3], "logits", 208),  # 4096 pairs: the one-block dispatch's limit
+    (700, 256, 1024, 8, 128, 1000, [3, 77], "logits", 209),  # 1002 slots x 22 chunks: separate scan
 ]
 
 
