@@ -95,6 +95,7 @@ def cpu_baseline(wl, n_tokens: int = 1536):
     logits = None if wl.logits is None else host(wl.logits)
     w13 = [host(wl.w13[s]) for s in range(wl.S)]
     w2 = [host(wl.w2[s]) for s in range(wl.S)]
+    n_tokens = min(n_tokens, wl.T)  # a decode batch is smaller than the sample: take all of it
     toks = sorted(np.random.default_rng(0).choice(wl.T, size=n_tokens, replace=False).tolist())
     t0 = time.perf_counter()
     _, _, ps, _ = O.ew_forward_tokens(toks, x, wg, logits, wl.k, ert, alive,
@@ -503,7 +504,7 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the expert-parallel "
-              "exchange across GPUs is not part of this build", file=sys.stderr)
+              "exchange across GPUs is not implemented", file=sys.stderr)
         sys.exit(2)
 
     import torch
