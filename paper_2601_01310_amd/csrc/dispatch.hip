@@ -12,7 +12,7 @@
 //   2. scan: per-slot totals, exclusive slot offsets, and the position of
 //      every (chunk, slot) within its slot in chunk order (the histograms
 //      are slot-major, so one wave scans one slot's chunks). When S times
-//      the number of chunks is at most 16384, each scatter block does this
+//      the number of chunks is at most 1024, each scatter block does this
 //      for itself from the whole histogram instead, and the launch is saved;
 //   3. scatter: each wave walks an equal share of a chunk in pair order and
 //      ranks the pairs of each group of 64 by slot: one ballot per bit of
@@ -33,7 +33,7 @@ namespace {
 
 constexpr int kMaxS = 1024;
 constexpr int kBlock = 256;
-constexpr long kFusedScanHist = 16384;  // S * nchunks up to which scatter scans by itself
+constexpr int kFusedScanHist = 1024;  // S * nchunks up to which scatter scans by itself
 
 // Slot of a pair of expert e: the first live ERT candidate of e.
 // REPLAY: -1 also when the first pass's slot pr is still alive (its result
@@ -229,21 +229,30 @@ __global__ __launch_bounds__(kBlock) void scatter_kernel(
   __shared__ int tot[SCAN ? kMaxS : 1];
   __shared__ int wsum[kWaves];
   for (int i = threadIdx.x; i < kWaves * kMaxS; i += kBlock) (&cnt[0][0])[i] = 0;
+  constexpr int kPer = SCAN ? kFusedScanHist / kBlock : 1;
+  int hv[kPer];
   if (SCAN) {
-    // Wave w takes slots w, w + 4, ...; lane l the chunks l, l + 64, ...
-    for (int s = wave; s < S; s += kWaves) {
-      const int32_t* hs = hist + (size_t)s * nchunks;
-      int all = 0, before = 0;
-      for (int c = lane; c < nchunks; c += kWave) {
-        const int v = hs[c];
-        all += v;
-        if (c < (int)blockIdx.x) before += v;
-      }
-      all = wave_sum_int(all);
-      before = wave_sum_int(before);
-      if (lane == 0) {
-        tot[s] = all;
-        base[s] = before;
+    // Thread i loads histogram entries i, i + 256, ... (all loads at once),
+    // and the slot totals and this chunk's positions are summed in LDS
+    // (integer atomics: the sums do not depend on their order).
+    const int nh = S * nchunks;
+#pragma unroll
+    for (int q = 0; q < kPer; ++q) {
+      const int j = threadIdx.x + q * kBlock;
+      hv[q] = j < nh ? hist[j] : 0;
+    }
+    for (int s = threadIdx.x; s < S; s += kBlock) {
+      tot[s] = 0;
+      base[s] = 0;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int q = 0; q < kPer; ++q) {
+      const int j = threadIdx.x + q * kBlock;
+      if (hv[q]) {
+        const int s = j / nchunks, c = j - s * nchunks;
+        atomicAdd(&tot[s], hv[q]);
+        if (c < (int)blockIdx.x) atomicAdd(&base[s], hv[q]);
       }
     }
   }
@@ -559,7 +568,7 @@ hipError_t remap_dispatch(bool replay, const int32_t* ids, int T, int k, const i
                          unserved_chunk, chunk);
   }
   // A small histogram is scanned by every scatter block (one launch less).
-  const bool fused_scan = nchunks > 0 && (long)S * nchunks <= kFusedScanHist;
+  const bool fused_scan = nchunks > 0 && (long)S * nchunks <= (long)kFusedScanHist;
   if (!fused_scan)
     hipLaunchKernelGGL(scan_kernel, dim3(1), dim3(1024), 0, stream, hist, unserved_chunk, nchunks,
                        S, counts, offsets, n_unserved, total_out);
