@@ -132,7 +132,7 @@ __global__ __launch_bounds__(kBlock) void remap_count_kernel(
 // w + 16, ...: lane l sums chunks 4l .. 4l+3, a wave scan gives every chunk
 // its exclusive position within the slot (written back in place, the
 // scatter adds the slot offset), and the slot totals go through a block
-// scan to the exclusive slot offsets.
+// scan (wave scans and the waves' totals) to the exclusive slot offsets.
 __global__ __launch_bounds__(1024) void scan_kernel(int32_t* __restrict__ hist,
                                                     const int32_t* __restrict__ unserved_chunk,
                                                     int nchunks, int S, int32_t* __restrict__ counts,
@@ -140,7 +140,7 @@ __global__ __launch_bounds__(1024) void scan_kernel(int32_t* __restrict__ hist,
                                                     int32_t* __restrict__ n_unserved,
                                                     int32_t* __restrict__ total_out) {
   __shared__ int tot[1024];
-  __shared__ int sc[2][1024];
+  __shared__ int wsum[1024 / kWave];
   __shared__ int nu;
   const int tid = threadIdx.x;
   const int wave = tid / kWave, lane = lane_id();
@@ -173,17 +173,18 @@ __global__ __launch_bounds__(1024) void scan_kernel(int32_t* __restrict__ hist,
   for (int c = tid; c < nchunks; c += 1024) part += unserved_chunk[c];
   __syncthreads();
   if (part) atomicAdd(&nu, part);
-  // Hillis-Steele inclusive scan over the slot totals.
+  // Inclusive scan over the slot totals: a wave scan per 64 slots, then the
+  // totals of the waves before.
   const int total = (tid < S) ? tot[tid] : 0;
-  sc[0][tid] = total;
-  __syncthreads();
-  int cur = 0;
-  for (int off = 1; off < 1024; off <<= 1) {
-    sc[cur ^ 1][tid] = sc[cur][tid] + (tid >= off ? sc[cur][tid - off] : 0);
-    cur ^= 1;
-    __syncthreads();
+  int incl = total;
+#pragma unroll
+  for (int off = 1; off < kWave; off <<= 1) {
+    const int t = __shfl_up(incl, off);
+    if (lane >= off) incl += t;
   }
-  const int incl = sc[cur][tid];
+  if (lane == kWave - 1) wsum[wave] = incl;
+  __syncthreads();
+  for (int w = 0; w < wave; ++w) incl += wsum[w];
   if (tid < S) {
     counts[tid] = total;
     offsets[tid] = incl - total;
