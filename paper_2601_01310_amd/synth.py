@@ -31,8 +31,9 @@ weights as its primary, §5.3).
 Expert weights are stored per slot: ``w13[s]`` is ``[2I, d]`` (rows 0..I-1
 the gate projection W1, rows I..2I-1 the up projection W3) and ``w2[s]`` is
 ``[d, I]``; both are (out, in) row-major bf16. The ERT is ``[E, R]`` int32,
-candidate slots in priority order (primary first), -1 padded; an expert with
-no local candidate is served by another EW.
+candidate slots in priority order (primary first, then the expert's shadows
+in slot order), -1 padded; an expert with no local candidate is served by
+another EW.
 """
 
 from __future__ import annotations
@@ -129,15 +130,25 @@ def zipf_bias(E: int, n_local: int, beta: float, seed: int) -> (torch.Tensor, Li
 
 
 def make_tables(E: int, n_local: int, shadow_experts: List[int]):
-    """ERT [E, 2] and slot->expert list: slot e holds local expert e (e < n_local),
-    slots n_local.. hold shadow copies of ``shadow_experts`` in order."""
+    """ERT [E, R] and slot->expert list: slot e holds local expert e (e < n_local),
+    slots n_local.. hold shadow copies of ``shadow_experts`` in order.
+
+    An expert's row lists its primary, then its shadows in slot order, then
+    -1; R is 1 + the largest number of shadows of any one expert (§4.2 lets
+    an expert map to one or more candidate locations)."""
     S = n_local + len(shadow_experts)
-    ert = torch.full((E, 2), -1, dtype=torch.int32)
+    n_shadow = [0] * E
+    for e in shadow_experts:
+        n_shadow[e] += 1
+    R = 1 + max(n_shadow + [0])
+    ert = torch.full((E, R), -1, dtype=torch.int32)
     for e in range(n_local):
         ert[e, 0] = e
     slot_expert = list(range(n_local))
+    col = [1] * E
     for i, e in enumerate(shadow_experts):
-        ert[e, 1] = n_local + i
+        ert[e, col[e]] = n_local + i
+        col[e] += 1
         slot_expert.append(e)
     return ert, slot_expert, S
 
@@ -179,7 +190,7 @@ def make_custom(T: int, d: int, E: int, k: int, I: int, n_local: int,
         w13[s].copy_(w13[slot_expert[s]])
         w2[s].copy_(w2[slot_expert[s]])
     alive = torch.ones(S, dtype=torch.uint8, device=device)
-    return Workload(name=name, T=T, d=d, E=E, k=k, I=I, S=S, R=2, x=x, wg=wg, logits=logits,
+    return Workload(name=name, T=T, d=d, E=E, k=k, I=I, S=S, R=int(ert.shape[1]), x=x, wg=wg, logits=logits,
                     ert=ert.to(device), alive=alive, w13=w13, w2=w2, slot_expert=slot_expert,
                     fail_experts=list(fail_experts or []), hot_experts=list(hot_experts or []))
 
