@@ -15,7 +15,8 @@
  *   - All tensor pointers are DEVICE pointers to dense row-major arrays.
  *     bf16 values travel as uint16_t bit patterns.
  *   - The caller owns every buffer; the library allocates nothing and keeps
- *     no state between calls.
+ *     no state between calls. (The one exception, tg_ew_forward_noalloc,
+ *     takes its workspace from a scratch area the library holds per GPU.)
  *   - Work is enqueued on `stream` (a hipStream_t; NULL = default stream)
  *     and is asynchronous: no call synchronises with the host. Data-dependent
  *     sizes (per-slot counts) stay on the device.
@@ -178,6 +179,28 @@ tg_status tg_ew_forward(const tg_ew_args* a, void* ws, size_t ws_bytes, void* st
  */
 tg_status tg_ew_forward_timed(const tg_ew_args* a, void* ws, size_t ws_bytes, void* stream,
                               void* const* events, int n_events);
+
+/*
+ * tg_ew_forward without a caller workspace, for callers that cannot
+ * allocate device memory: code under HIP graph capture, serving loops and
+ * harnesses that must not call the allocator. It computes what tg_ew_forward
+ * computes, with the same kernels in the same order, and allocates nothing:
+ * its workspace is a scratch area of TG_NOALLOC_SCRATCH_BYTES that the
+ * library holds on each GPU it runs on, until the process ends.
+ *
+ * A batch whose tg_ew_forward_workspace(a) exceeds TG_NOALLOC_SCRATCH_BYTES
+ * is rejected with TG_ERR_WORKSPACE before anything is enqueued (a caller
+ * buffer in a->y keeps the per-pair outputs out of the scratch area; 64 MiB
+ * covers, e.g., a decode step of 432 tokens at DeepSeek-V3 expert shapes).
+ * The first call on a device resolves that device's scratch address, which
+ * may load the library's device code there: make it outside graph capture.
+ * All calls on one GPU share its scratch area, which keeps the last call's
+ * contents (nothing in it has to start at zero): calls that may overlap on
+ * one GPU (streams with no ordering between them, concurrent host threads)
+ * race and must be serialised by the caller.
+ */
+#define TG_NOALLOC_SCRATCH_BYTES (64u * 1024u * 1024u)
+tg_status tg_ew_forward_noalloc(const tg_ew_args* a, void* stream);
 
 /*
  * Replay of failed pairs (§5.1): after a forward, slots may fail (or be

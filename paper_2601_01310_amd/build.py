@@ -25,7 +25,7 @@ DEVICE = [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-p
           "-munsafe-fp-atomics"]
 
 SOURCES = ["gate_topk.hip", "dispatch.hip", "grouped_gemm.hip", "combine.hip", "trigger.hip",
-           "kv_checkpoint.hip",
+           "kv_checkpoint.hip", "noalloc.hip",
            "tg_api.cpp"]
 
 

@@ -13,13 +13,18 @@ namespace {
 
 thread_local std::string g_last_error;
 
-tg_status fail(tg_status s, const char* fmt, ...) {
+tg_status vfail(tg_status s, const char* fmt, va_list ap) {
   char buf[512];
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  g_last_error = buf;
+  return s;
+}
+
+tg_status fail(tg_status s, const char* fmt, ...) {
   va_list ap;
   va_start(ap, fmt);
-  vsnprintf(buf, sizeof(buf), fmt, ap);
+  vfail(s, fmt, ap);
   va_end(ap);
-  g_last_error = buf;
   return s;
 }
 
@@ -168,7 +173,89 @@ ReplayLayout replay_layout(const tg_replay_args* a, char* base) {
   return L;
 }
 
+tg_status check_ew(const tg_ew_args* a) {
+  if (!a) return fail(TG_ERR_NULL_ARG, "args is NULL");
+  tg_status st = check_gate_dims(a->T, a->E, a->k);
+  if (st != TG_OK) return st;
+  if ((st = check_ffn(a->d, a->I)) != TG_OK) return st;
+  if ((st = check_slots(a->S, a->R)) != TG_OK) return st;
+  if (!a->x || !a->ert || !a->slot_alive || !a->w13 || !a->w2 || !a->out)
+    return fail(TG_ERR_NULL_ARG, "a required pointer is NULL");
+  if ((a->w_gate == nullptr) == (a->logits_in == nullptr))
+    return fail(TG_ERR_NULL_ARG, "give exactly one of w_gate and logits_in");
+  return TG_OK;
+}
+
 }  // namespace
+
+namespace tg {
+
+tg_status ew_forward(const tg_ew_args* a, void* ws, size_t ws_bytes, void* stream,
+                     void* const* events) {
+  tg_status st = check_ew(a);
+  if (st != TG_OK) return st;
+  const size_t need = ew_layout(a, nullptr).bytes;
+  if (!ws || ws_bytes < need)
+    return fail(TG_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need, ws_bytes);
+  if (reinterpret_cast<uintptr_t>(ws) & 255)
+    return fail(TG_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  EwLayout L = ew_layout(a, static_cast<char*>(ws));
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  int32_t* ids = a->topk_ids ? a->topk_ids : L.ids;
+  float* w = a->topk_w ? a->topk_w : L.w;
+  int32_t* pair_slot = a->pair_slot ? a->pair_slot : L.pair_slot;
+  int32_t* counts = a->slot_counts ? a->slot_counts : L.counts;
+  int32_t* offsets = a->slot_offsets ? a->slot_offsets : L.offsets;
+  int32_t* pair_row = a->pair_row ? a->pair_row : L.pair_row;
+  int32_t* n_unserved = a->n_unserved ? a->n_unserved : L.n_unserved;
+  const int max_rows = a->T * a->k;
+  hipError_t e = hipSuccess;
+  auto mark = [&](int i) {
+    if (events && e == hipSuccess) e = hipEventRecord(static_cast<hipEvent_t>(events[i]), s);
+  };
+  mark(0);
+  if (e == hipSuccess)
+    e = tg::launch_gate_topk(a->w_gate ? a->x : nullptr, a->w_gate, a->logits_in, a->T, a->d, a->E,
+                             a->k, nullptr, ids, w, s);
+  mark(1);
+  // The gate/up GEMM reads the token rows in place through perm when x is
+  // addressable with 32-bit byte offsets; otherwise they are gathered first.
+  const bool in_place = 2LL * a->T * a->d < (1LL << 31);
+  if (e == hipSuccess)
+    e = tg::launch_remap_dispatch(ids, a->T, a->k, a->ert, a->E, a->R, a->slot_alive, a->S,
+                                  in_place ? nullptr : a->x, a->d, pair_slot, counts, offsets,
+                                  L.perm, pair_row, in_place ? nullptr : L.x_perm, n_unserved,
+                                  L.dispatch_ws, s, a->token_valid);
+  mark(2);
+  if (e == hipSuccess)
+    e = in_place ? tg::launch_ffn_gateup_gather(a->x, a->T, L.perm, a->k, offsets, a->S, max_rows,
+                                                a->w13, a->d, a->I, L.h, s)
+                 : tg::launch_ffn_gateup(L.x_perm, offsets, a->S, max_rows, a->w13, a->d, a->I,
+                                         L.h, s);
+  mark(3);
+  if (e == hipSuccess)
+    e = tg::launch_ffn_down(L.h, offsets, a->S, max_rows, a->w2, a->d, a->I, L.y, s);
+  mark(4);
+  if (e == hipSuccess) e = tg::launch_combine(L.y, pair_row, w, a->T, a->k, a->d, a->out, s);
+  mark(5);
+  return hip_status(e, "tg_ew_forward");
+}
+
+tg_status ew_check(const tg_ew_args* a, size_t* ws_bytes) {
+  const tg_status st = check_ew(a);
+  if (st == TG_OK) *ws_bytes = ew_layout(a, nullptr).bytes;
+  return st;
+}
+
+tg_status set_error(tg_status s, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vfail(s, fmt, ap);
+  va_end(ap);
+  return s;
+}
+
+}  // namespace tg
 
 extern "C" {
 
@@ -264,77 +351,13 @@ tg_status tg_combine(const uint16_t* y, const int32_t* pair_row, const float* to
       "tg_combine");
 }
 
-static tg_status check_ew(const tg_ew_args* a) {
-  if (!a) return fail(TG_ERR_NULL_ARG, "args is NULL");
-  tg_status st = check_gate_dims(a->T, a->E, a->k);
-  if (st != TG_OK) return st;
-  if ((st = check_ffn(a->d, a->I)) != TG_OK) return st;
-  if ((st = check_slots(a->S, a->R)) != TG_OK) return st;
-  if (!a->x || !a->ert || !a->slot_alive || !a->w13 || !a->w2 || !a->out)
-    return fail(TG_ERR_NULL_ARG, "a required pointer is NULL");
-  if ((a->w_gate == nullptr) == (a->logits_in == nullptr))
-    return fail(TG_ERR_NULL_ARG, "give exactly one of w_gate and logits_in");
-  return TG_OK;
-}
-
 size_t tg_ew_forward_workspace(const tg_ew_args* a) {
   if (check_ew(a) != TG_OK) return 0;
   return ew_layout(a, nullptr).bytes;
 }
 
-static tg_status ew_forward(const tg_ew_args* a, void* ws, size_t ws_bytes, void* stream,
-                            void* const* events) {
-  tg_status st = check_ew(a);
-  if (st != TG_OK) return st;
-  const size_t need = ew_layout(a, nullptr).bytes;
-  if (!ws || ws_bytes < need)
-    return fail(TG_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need, ws_bytes);
-  if (reinterpret_cast<uintptr_t>(ws) & 255)
-    return fail(TG_ERR_WORKSPACE, "workspace must be 256-byte aligned");
-  EwLayout L = ew_layout(a, static_cast<char*>(ws));
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  int32_t* ids = a->topk_ids ? a->topk_ids : L.ids;
-  float* w = a->topk_w ? a->topk_w : L.w;
-  int32_t* pair_slot = a->pair_slot ? a->pair_slot : L.pair_slot;
-  int32_t* counts = a->slot_counts ? a->slot_counts : L.counts;
-  int32_t* offsets = a->slot_offsets ? a->slot_offsets : L.offsets;
-  int32_t* pair_row = a->pair_row ? a->pair_row : L.pair_row;
-  int32_t* n_unserved = a->n_unserved ? a->n_unserved : L.n_unserved;
-  const int max_rows = a->T * a->k;
-  hipError_t e = hipSuccess;
-  auto mark = [&](int i) {
-    if (events && e == hipSuccess) e = hipEventRecord(static_cast<hipEvent_t>(events[i]), s);
-  };
-  mark(0);
-  if (e == hipSuccess)
-    e = tg::launch_gate_topk(a->w_gate ? a->x : nullptr, a->w_gate, a->logits_in, a->T, a->d, a->E,
-                             a->k, nullptr, ids, w, s);
-  mark(1);
-  // The gate/up GEMM reads the token rows in place through perm when x is
-  // addressable with 32-bit byte offsets; otherwise they are gathered first.
-  const bool in_place = 2LL * a->T * a->d < (1LL << 31);
-  if (e == hipSuccess)
-    e = tg::launch_remap_dispatch(ids, a->T, a->k, a->ert, a->E, a->R, a->slot_alive, a->S,
-                                  in_place ? nullptr : a->x, a->d, pair_slot, counts, offsets,
-                                  L.perm, pair_row, in_place ? nullptr : L.x_perm, n_unserved,
-                                  L.dispatch_ws, s, a->token_valid);
-  mark(2);
-  if (e == hipSuccess)
-    e = in_place ? tg::launch_ffn_gateup_gather(a->x, a->T, L.perm, a->k, offsets, a->S, max_rows,
-                                                a->w13, a->d, a->I, L.h, s)
-                 : tg::launch_ffn_gateup(L.x_perm, offsets, a->S, max_rows, a->w13, a->d, a->I,
-                                         L.h, s);
-  mark(3);
-  if (e == hipSuccess)
-    e = tg::launch_ffn_down(L.h, offsets, a->S, max_rows, a->w2, a->d, a->I, L.y, s);
-  mark(4);
-  if (e == hipSuccess) e = tg::launch_combine(L.y, pair_row, w, a->T, a->k, a->d, a->out, s);
-  mark(5);
-  return hip_status(e, "tg_ew_forward");
-}
-
 tg_status tg_ew_forward(const tg_ew_args* a, void* ws, size_t ws_bytes, void* stream) {
-  return ew_forward(a, ws, ws_bytes, stream, nullptr);
+  return tg::ew_forward(a, ws, ws_bytes, stream, nullptr);
 }
 
 tg_status tg_ew_forward_timed(const tg_ew_args* a, void* ws, size_t ws_bytes, void* stream,
@@ -343,7 +366,7 @@ tg_status tg_ew_forward_timed(const tg_ew_args* a, void* ws, size_t ws_bytes, vo
   if (n_events != 6) return fail(TG_ERR_BAD_DIM, "n_events=%d, 6 required", n_events);
   for (int i = 0; i < 6; ++i)
     if (!events[i]) return fail(TG_ERR_NULL_ARG, "events[%d] is NULL", i);
-  return ew_forward(a, ws, ws_bytes, stream, events);
+  return tg::ew_forward(a, ws, ws_bytes, stream, events);
 }
 
 static tg_status check_replay(const tg_replay_args* a) {

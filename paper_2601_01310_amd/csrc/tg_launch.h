@@ -10,6 +10,15 @@
 
 namespace tg {
 
+// C-ABI internals (tg_api.cpp) shared with the no-allocation forward
+// (noalloc.hip): argument validation with the workspace size it implies,
+// the checked forward on a given workspace, and the thread-local error
+// detail that tg_last_error() reports.
+tg_status ew_check(const tg_ew_args* a, size_t* ws_bytes);
+tg_status ew_forward(const tg_ew_args* a, void* ws, size_t ws_bytes, void* stream,
+                     void* const* events);
+tg_status set_error(tg_status s, const char* fmt, ...);
+
 hipError_t launch_gate_topk(const uint16_t* x, const uint16_t* wg, const float* logits_in, int T,
                             int d, int E, int k, float* logits_out, int32_t* ids, float* w,
                             hipStream_t stream);

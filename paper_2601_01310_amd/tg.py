@@ -21,7 +21,7 @@ TG_OK, TG_ERR_NULL_ARG, TG_ERR_BAD_DIM, TG_ERR_UNSUPPORTED, TG_ERR_WORKSPACE, TG
 EXPORTS = [
     "tg_status_string", "tg_last_error", "tg_gate_topk", "tg_remap_dispatch_workspace",
     "tg_remap_dispatch", "tg_expert_ffn_grouped", "tg_combine", "tg_ew_forward_workspace",
-    "tg_ew_forward", "tg_ew_forward_timed", "tg_ew_replay_workspace", "tg_ew_replay",
+    "tg_ew_forward", "tg_ew_forward_timed", "tg_ew_forward_noalloc", "tg_ew_replay_workspace", "tg_ew_replay",
     "tg_batch_trigger", "tg_kv_checkpoint", "tg_kv_checkpoint_strided", "tg_kv_restore",
 ]
 
@@ -86,6 +86,8 @@ def load(path: Optional[str] = None):
     lib.tg_ew_forward_timed.restype = i
     lib.tg_ew_forward_timed.argtypes = [ctypes.POINTER(EwArgs), vp, sz, vp,
                                         ctypes.POINTER(ctypes.c_void_p), i]
+    lib.tg_ew_forward_noalloc.restype = i
+    lib.tg_ew_forward_noalloc.argtypes = [ctypes.POINTER(EwArgs), vp]
     lib.tg_ew_replay_workspace.restype = sz
     lib.tg_ew_replay_workspace.argtypes = [ctypes.POINTER(ReplayArgs)]
     lib.tg_ew_replay.restype = i
@@ -192,6 +194,16 @@ def tg_ew_forward_workspace(args: EwArgs) -> int:
 def tg_ew_forward(args: EwArgs, ws, ws_bytes, stream=None):
     _check(load().tg_ew_forward(ctypes.byref(args), _p(ws), ws_bytes, _stream(stream)),
            "tg_ew_forward")
+
+
+# Bytes of the library's own scratch area behind tg_ew_forward_noalloc
+# (TG_NOALLOC_SCRATCH_BYTES in tg.h).
+NOALLOC_SCRATCH_BYTES = 64 * 1024 * 1024
+
+
+def tg_ew_forward_noalloc(args: EwArgs, stream=None):
+    _check(load().tg_ew_forward_noalloc(ctypes.byref(args), _stream(stream)),
+           "tg_ew_forward_noalloc")
 
 
 def tg_ew_forward_timed(args: EwArgs, ws, ws_bytes, events, stream=None):
