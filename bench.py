@@ -3,7 +3,10 @@
 One step is one tg_ew_forward call (gating, ERT remap and dispatch, grouped
 SwiGLU expert FFN, combine) over the Mixtral-shaped workload: T=4096 tokens,
 d=4096, E=8 experts, top-2, I=14336, 8 primary + 2 shadow slots, synthetic
-bf16 inputs already resident in HBM. Prints one JSON line.
+bf16 inputs already resident in HBM. Prints one JSON line; its "workloads"
+key carries the same measurement, compact, for the DeepSeek-V3 expert share
+(T=16384, d=7168, 256 experts, top-8, I=2048, 32 + 8 slots), its skewed
+failover variant and the decode-size batch (T=128).
 
   python bench.py [--gpus 1] [--steps 20] [--warmup 3] [--workload mixtral]
 """
@@ -102,10 +105,31 @@ def cpu_baseline(wl, n_tokens: int = 1536):
                                       lambda s: w13[s], lambda s: w2[s])
     dt = time.perf_counter() - t0
     pairs = int((ps >= 0).sum())
-    threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
-    return {"value": pairs / dt, "unit": "routed pairs/s", "cores": int(threads), "kind": "oracle",
+    blas = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    cores, model = host_cpu()
+    return {"value": pairs / dt, "unit": "routed pairs/s", "cores": int(min(blas, cores)),
+            "kind": "oracle",
             "sample": f"{n_tokens} seeded tokens of the workload ({pairs} routed pairs), float64 "
-                      f"per-token oracle incl. widening the touched slots' bf16 weights; {dt:.1f} s"}
+                      f"per-token oracle incl. widening the touched slots' bf16 weights; {dt:.1f} s",
+            "host_cores": cores, "blas_threads": int(blas), "cpu_model": model}
+
+
+def host_cpu():
+    """CPUs this process may run on (nproc) and the CPU model name."""
+    try:
+        cores = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        cores = os.cpu_count() or 1
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for ln in fh:
+                if ln.startswith("model name"):
+                    model = ln.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return cores, model
 
 
 def _ffn_buffers(d, I, S, max_rows, dev, seed=0):
@@ -473,6 +497,136 @@ def measured_peaks(dev):
                    "bf16 matrix (4 GiB read); copy of 2 GiB (read + write bytes); best of 5"}
 
 
+OTHER_WORKLOADS = ["dsv3_share", "dsv3_skew", "dsv3_decode"]
+FAILOVER_BLOCKS = 8          # healthy / rerouted blocks, interleaved
+FAILOVER_BLOCK_STEPS = 20    # at least this many steps per block
+
+
+def _pct(v, q):
+    v = sorted(v)
+    return v[min(len(v) - 1, int(q * (len(v) - 1) + 0.5))]
+
+
+def measure_workload(wl, alive, steps, warmup, with_failover=True):
+    """Times tg_ew_forward on one resident workload: ``steps`` plain steps
+    (host clock around the loop, one hipEvent after each step on the call's
+    stream), a second pass through tg_ew_forward_timed for the per-stage
+    means, the roofline of the dominant kernel (the gate/up GEMM), and, when
+    the workload has a failure configuration, healthy and rerouted steps in
+    interleaved blocks."""
+    import torch
+
+    from paper_2601_01310_amd import tg
+
+    f = tg.EwForward(wl, alive)
+    hip = HipEvents()
+    stream = torch.cuda.current_stream()
+
+    def timed_steps(n):
+        evs = hip.create(n + 1)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        hip.record(evs[0], stream)
+        for i in range(n):
+            tg.tg_ew_forward(f.args, f.ws, f.ws_bytes, stream)
+            hip.record(evs[i + 1], stream)
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        per = sorted(hip.elapsed_ms(evs[i], evs[i + 1]) for i in range(n))
+        hip.destroy(evs)
+        return per, (t1 - t0) * 1e3 / n
+
+    def stage_times(n):
+        evs = hip.create(6 * n)
+        torch.cuda.synchronize()
+        for i in range(n):
+            tg.tg_ew_forward_timed(f.args, f.ws, f.ws_bytes, evs[6 * i:6 * i + 6], stream)
+        torch.cuda.synchronize()
+        st = [sum(hip.elapsed_ms(evs[6 * i + j], evs[6 * i + j + 1]) for i in range(n)) / n
+              for j in range(5)]
+        hip.destroy(evs)
+        return st
+
+    for _ in range(warmup):
+        f(stream)
+    step_ev, ms = timed_steps(steps)
+    stage_ms = stage_times(steps)
+    P = int(f.slot_offsets[-1])
+    counts = f.slot_counts.cpu()
+    touched = int((counts > 0).sum())
+
+    failover = None
+    fail_alive = wl.alive_after_failure()
+    if with_failover and not torch.equal(fail_alive, wl.alive):
+        # Healthy and rerouted configurations alternate in blocks, so that
+        # both see the same clock and temperature; p50 and the inter-quartile
+        # range of each, and the cost with its own spread.
+        n = max(steps, FAILOVER_BLOCK_STEPS)
+        per = {"healthy": [], "failover": []}
+        for _ in range(FAILOVER_BLOCKS // 2):
+            for tag, al in (("healthy", wl.alive), ("failover", fail_alive)):
+                f.set_alive(al)
+                for _ in range(2):
+                    f(stream)
+                per[tag] += timed_steps(n)[0]
+        f.set_alive(fail_alive)
+        f(stream)
+        torch.cuda.synchronize()
+        fo_pairs = int(f.slot_offsets[-1])
+        f.set_alive(alive)
+        q = {t: (_pct(v, 0.25), _pct(v, 0.5), _pct(v, 0.75)) for t, v in per.items()}
+        h, fo = q["healthy"], q["failover"]
+        failover = {"step_ms_p50": fo[1], "step_ms_iqr": [fo[0], fo[2]],
+                    "healthy_step_ms_p50": h[1], "healthy_step_ms_iqr": [h[0], h[2]],
+                    "cost": fo[1] / h[1] - 1.0,
+                    "cost_spread": (h[2] - h[0]) / h[1],
+                    "routed_pairs": fo_pairs, "blocks": FAILOVER_BLOCKS, "steps_per_block": n}
+
+    d, I = wl.d, wl.I
+    gemm1_flop = 4.0 * d * I * P
+    gemm1_s = stage_ms[2] * 1e-3
+    # Algorithmic bytes of the gate/up GEMM: the touched slots' W1/W3, the
+    # routed rows of x and h.
+    gemm1_bytes = touched * 2.0 * I * d * 2 + P * d * 2.0 + P * I * 2.0
+    if gemm1_flop / max(gemm1_bytes, 1.0) >= RIDGE_FLOP_PER_BYTE:
+        achieved = gemm1_flop / gemm1_s / 1e12
+        roof = {"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
+                "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS}
+    else:
+        achieved = gemm1_bytes / gemm1_s / 1e9
+        roof = {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": achieved / PEAK_HBM_GBS}
+    roof = {"bound": roof["bound"], "kernel": "grouped_gemm gate/up + SwiGLU", **roof}
+    p50 = step_ev[len(step_ev) // 2]
+    # Bytes the whole step must stream: every touched slot's three weight
+    # matrices, the token rows and the outputs.
+    step_bytes = touched * 3.0 * I * d * 2 + wl.T * d * 2.0 * 2
+    return {"routed_pairs": P, "touched_slots": touched, "pairs_per_s": P / (ms * 1e-3),
+            "ms_per_step": ms, "step_ms_p50": p50, "step_ms_mean": sum(step_ev) / len(step_ev),
+            "stages_ms": dict(zip(STAGES, stage_ms)), "roofline": roof,
+            "expert_ffn_tflops": 6.0 * d * I * P / ((stage_ms[2] + stage_ms[3]) * 1e-3) / 1e12,
+            "step_flop_frac": 6.0 * d * I * P / (p50 * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
+            "step_hbm_frac": step_bytes / (p50 * 1e-3) / 1e9 / PEAK_HBM_GBS,
+            "failover": failover}
+
+
+def compact(wl, r):
+    """The summary of one extra workload carried in the benchmark line."""
+    out = {"workload": f"T={wl.T} d={wl.d} E={wl.E} top-{wl.k} I={wl.I} slots={wl.S}",
+           "routed_pairs": r["routed_pairs"], "touched_slots": r["touched_slots"],
+           "pairs_per_s": r["pairs_per_s"], "step_ms_p50": r["step_ms_p50"],
+           "ms_per_step": r["ms_per_step"],
+           "stages_ms": {k: round(v, 4) for k, v in r["stages_ms"].items()},
+           "roofline": r["roofline"]}
+    if r["roofline"]["bound"] == "hbm":
+        out["step_hbm_frac"] = r["step_hbm_frac"]
+    else:
+        out["step_flop_frac"] = r["step_flop_frac"]
+    if r["failover"] is not None:
+        out["failover"] = r["failover"]
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -482,6 +636,9 @@ def main():
     ap.add_argument("--failover", action="store_true",
                     help="time the run with the workload's failed primaries rerouted to shadows")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-others", action="store_true",
+                    help="time only the named workload (by default the mixtral line also carries "
+                         "the DeepSeek-V3 share, skewed and decode workloads under 'workloads')")
     ap.add_argument("--knee", action="store_true",
                     help="expert FFN time against the expert batch size (prints one JSON line per "
                          "point instead of the benchmark line)")
@@ -538,96 +695,17 @@ def main():
         checkpoint_cost(wl, args.steps, args.warmup)
         return
     alive = wl.alive_after_failure() if args.failover else wl.alive
-    f = tg.EwForward(wl, alive)
-    hip = HipEvents()
-    stream = torch.cuda.current_stream()
-
-    def timed_steps(n):
-        """n plain steps of the whole path: host wall time per step and the
-        sorted per-step times from one pair of events around each step."""
-        evs = hip.create(n + 1)
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        hip.record(evs[0], stream)
-        for i in range(n):
-            tg.tg_ew_forward(f.args, f.ws, f.ws_bytes, stream)
-            hip.record(evs[i + 1], stream)
-        torch.cuda.synchronize()
-        t1 = time.perf_counter()
-        per = sorted(hip.elapsed_ms(evs[i], evs[i + 1]) for i in range(n))
-        hip.destroy(evs)
-        return per, (t1 - t0) * 1e3 / n
-
-    def stage_times(n):
-        """Mean per-stage times over n steps with events between the stages
-        (a separate pass: the events add a little time between kernels)."""
-        evs = hip.create(6 * n)
-        torch.cuda.synchronize()
-        for i in range(n):
-            tg.tg_ew_forward_timed(f.args, f.ws, f.ws_bytes, evs[6 * i:6 * i + 6], stream)
-        torch.cuda.synchronize()
-        st = [sum(hip.elapsed_ms(evs[6 * i + j], evs[6 * i + j + 1]) for i in range(n)) / n
-              for j in range(5)]
-        hip.destroy(evs)
-        return st
-
-    for _ in range(args.warmup):
-        f(stream)
-    step_ev, ms = timed_steps(args.steps)
-    stage_ms = stage_times(args.steps)
-    P = int(f.slot_offsets[-1])
-    counts = f.slot_counts.cpu()
-    touched = int((counts > 0).sum())
-
-    failover = None
-    if not args.failover and not torch.equal(wl.alive_after_failure(), wl.alive):
-        # The same inputs with the workload's failed primaries rerouted to
-        # their shadows: the rerouted run should cost the same. The two
-        # configurations alternate in four blocks of steps, so that both see
-        # the same clock (the GPU runs hotter after the timed loop above).
-        fail_alive, n = wl.alive_after_failure(), max(args.steps // 4, 1)
-        per = {"healthy": [], "failover": []}
-        for _ in range(2):
-            for tag, al in (("healthy", wl.alive), ("failover", fail_alive)):
-                f.set_alive(al)
-                for _ in range(max(args.warmup // 2, 1)):
-                    f(stream)
-                per[tag] += timed_steps(n)[0]
-        f.set_alive(fail_alive)
-        f(stream)
-        torch.cuda.synchronize()
-        fo_pairs = int(f.slot_offsets[-1])
-        f.set_alive(wl.alive)
-        med = {t: sorted(v)[len(v) // 2] for t, v in per.items()}
-        failover = {"step_ms_p50": med["failover"], "healthy_step_ms_p50": med["healthy"],
-                    "cost": med["failover"] / med["healthy"] - 1.0, "routed_pairs": fo_pairs,
-                    "steps_each": 2 * n}
-
+    res = measure_workload(wl, alive, args.steps, args.warmup, with_failover=not args.failover)
+    P, touched, stage_ms = res["routed_pairs"], res["touched_slots"], res["stages_ms"]
     d, I = wl.d, wl.I
-    gemm1_flop = 4.0 * d * I * P
-    gemm1_s = stage_ms[2] * 1e-3
-    # Algorithmic bytes of the gate/up GEMM: the touched slots' W1/W3, the
-    # routed rows of x and h.
-    gemm1_bytes = touched * 2.0 * I * d * 2 + P * d * 2.0 + P * I * 2.0
-    if gemm1_flop / max(gemm1_bytes, 1.0) >= RIDGE_FLOP_PER_BYTE:
-        achieved = gemm1_flop / gemm1_s / 1e12
-        roof = {"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
-                "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS}
-    else:
-        achieved = gemm1_bytes / gemm1_s / 1e9
-        roof = {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                "frac": achieved / PEAK_HBM_GBS}
-    roof = {"bound": roof["bound"], "kernel": "grouped_gemm gate/up + SwiGLU", **roof,
-            "traffic": measured_traffic(args.workload)}
-    ffn_tflops = 6.0 * d * I * P / ((stage_ms[2] + stage_ms[3]) * 1e-3) / 1e12
     line = {
         "metric": "routed token-expert pairs/sec for EW forward",
-        "value": P / (ms * 1e-3),
+        "value": res["pairs_per_s"],
         "unit": "pairs/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": ms,
+        "ms_per_step": res["ms_per_step"],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -636,20 +714,31 @@ def main():
         "config": {"workload": f"{args.workload}: T={wl.T} d={d} E={wl.E} top-{wl.k} I={I} "
                                f"slots={wl.S}" + (" failover" if args.failover else ""),
                    "routed_pairs": P, "touched_slots": touched},
-        "roofline": roof,
-        "step_ms_p50": step_ev[len(step_ev) // 2],
-        "step_ms_mean": sum(step_ev) / len(step_ev),
-        "stages_ms": dict(zip(STAGES, stage_ms)),
-        "expert_ffn_tflops": ffn_tflops,
+        "roofline": dict(res["roofline"], traffic=measured_traffic(args.workload)),
+        "step_ms_p50": res["step_ms_p50"],
+        "step_ms_mean": res["step_ms_mean"],
+        "stages_ms": stage_ms,
+        "expert_ffn_tflops": res["expert_ffn_tflops"],
     }
+    if res.get("failover") is not None:
+        line["failover"] = res["failover"]
+    if not args.no_others and args.workload == "mixtral" and not args.failover:
+        # The other full-size workloads, each timed the same way (compact).
+        line["workloads"] = {}
+        for name in OTHER_WORKLOADS:
+            wl2 = synth.make(name, device=dev)
+            r2 = measure_workload(wl2, wl2.alive, max(args.steps, 20), args.warmup,
+                                  with_failover=True)
+            line["workloads"][name] = compact(wl2, r2)
+            del wl2
+            torch.cuda.empty_cache()
     if not args.no_peaks:
         mp = measured_peaks(dev)
+        roof = line["roofline"]
         ref = (mp["bf16_gemm_tflops"] if roof["bound"] == "mfma"
                else max(mp["hbm_read_tbps"], mp["hbm_copy_tbps"]) * 1e3)
         line["measured_peaks"] = mp
         line["roofline"]["frac_of_measured"] = roof["achieved"] / ref
-    if failover is not None:
-        line["failover"] = failover
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(wl)
     print(json.dumps(line), flush=True)
