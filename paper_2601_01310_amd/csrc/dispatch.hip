@@ -105,7 +105,7 @@ __global__ __launch_bounds__(kBlock) void remap_count_kernel(
     const int32_t* __restrict__ ids, int npairs, int k, const int32_t* __restrict__ ert, int E,
     int R, const uint8_t* __restrict__ alive, int S, const uint8_t* __restrict__ token_valid,
     const int32_t* __restrict__ prior, int32_t* __restrict__ out_slot, int32_t* __restrict__ hist,
-    int32_t* __restrict__ unserved_chunk, int chunk) {
+    int32_t* __restrict__ unserved_chunk, int chunk, uint32_t* __restrict__ zero, int zero_words) {
   __shared__ int h[kMaxS];
   __shared__ int nu;
   for (int s = threadIdx.x; s < S; s += kBlock) h[s] = 0;
@@ -125,6 +125,9 @@ __global__ __launch_bounds__(kBlock) void remap_count_kernel(
   __syncthreads();
   for (int s = threadIdx.x; s < S; s += kBlock) hist[(size_t)s * gridDim.x + blockIdx.x] = h[s];
   if (threadIdx.x == 0) unserved_chunk[blockIdx.x] = nu;
+  // The GEMMs' schedule area of this call starts at zero.
+  if (zero && blockIdx.x == 0)
+    for (int i = threadIdx.x; i < zero_words; i += kBlock) zero[i] = 0;
 }
 
 // One block of 1024 threads (16 waves). hist[s * nchunks + c] holds the
@@ -357,7 +360,7 @@ __global__ __launch_bounds__(kOneBlock) void dispatch_one_block_kernel(
     const uint8_t* __restrict__ token_valid, const int32_t* __restrict__ prior,
     int32_t* __restrict__ out_slot, int32_t* __restrict__ counts, int32_t* __restrict__ offsets,
     int32_t* __restrict__ perm, int32_t* __restrict__ pair_row, int32_t* __restrict__ n_unserved,
-    int32_t* __restrict__ total_out) {
+    int32_t* __restrict__ total_out, uint32_t* __restrict__ zero, int zero_words) {
   constexpr int kWaves = kOneBlock / kWave;
   // cnt[w][s]: pairs of wave w on slot s in the current group of 1024, then
   // their first row; 0 wherever wave w has no pair on s.
@@ -491,6 +494,9 @@ __global__ __launch_bounds__(kOneBlock) void dispatch_one_block_kernel(
       if (my_row[i] >= 0) perm[my_row[i]] = p;
     }
   }
+  // The GEMMs' schedule area of this call starts at zero.
+  if (zero)
+    for (int j = tid; j < zero_words; j += kOneBlock) zero[j] = 0;
 }
 
 __global__ __launch_bounds__(kBlock) void gather_kernel(const uint4* __restrict__ x,
@@ -530,7 +536,9 @@ hipError_t remap_dispatch(bool replay, const int32_t* ids, int T, int k, const i
                           const int32_t* prior, const uint16_t* x, int d, int32_t* pair_slot,
                           int32_t* counts, int32_t* offsets, int32_t* perm, int32_t* pair_row,
                           uint16_t* x_perm, int32_t* n_unserved, int32_t* total_out, void* ws,
-                          hipStream_t stream) {
+                          hipStream_t stream, void* sched_area) {
+  uint32_t* const zero = static_cast<uint32_t*>(sched_area);
+  const int zero_words = sched_area ? (int)(kSchedBytes / 4) : 0;
   const int npairs = T * k;
   const int chunk = dispatch_chunk(npairs);
   const int nchunks = (npairs + chunk - 1) / chunk;
@@ -542,11 +550,12 @@ hipError_t remap_dispatch(bool replay, const int32_t* ids, int T, int k, const i
     if (replay)
       hipLaunchKernelGGL(dispatch_one_block_kernel<true>, dim3(1), dim3(kOneBlock), 0, stream, ids,
                          npairs, k, ert, E, R, alive, S, sbits, nullptr, prior, pair_slot, counts,
-                         offsets, perm, pair_row, n_unserved, total_out);
+                         offsets, perm, pair_row, n_unserved, total_out, zero, zero_words);
     else
       hipLaunchKernelGGL(dispatch_one_block_kernel<false>, dim3(1), dim3(kOneBlock), 0, stream,
                          ids, npairs, k, ert, E, R, alive, S, sbits, token_valid, nullptr,
-                         pair_slot, counts, offsets, perm, pair_row, n_unserved, total_out);
+                         pair_slot, counts, offsets, perm, pair_row, n_unserved, total_out, zero,
+                         zero_words);
     if (x_perm && npairs > 0) {
       const int nch = d / 8;
       const long maxq = (long)npairs * nch;
@@ -562,11 +571,11 @@ hipError_t remap_dispatch(bool replay, const int32_t* ids, int T, int k, const i
     if (replay)
       hipLaunchKernelGGL(remap_count_kernel<true>, dim3(nchunks), dim3(kBlock), 0, stream, ids,
                          npairs, k, ert, E, R, alive, S, nullptr, prior, pair_slot, hist,
-                         unserved_chunk, chunk);
+                         unserved_chunk, chunk, zero, zero_words);
     else
       hipLaunchKernelGGL(remap_count_kernel<false>, dim3(nchunks), dim3(kBlock), 0, stream, ids,
                          npairs, k, ert, E, R, alive, S, token_valid, nullptr, pair_slot, hist,
-                         unserved_chunk, chunk);
+                         unserved_chunk, chunk, zero, zero_words);
   }
   // A small histogram is scanned by every scatter block (one launch less).
   const bool fused_scan = nchunks > 0 && (long)S * nchunks <= (long)kFusedScanHist;
@@ -602,10 +611,10 @@ hipError_t launch_remap_dispatch(const int32_t* ids, int T, int k, const int32_t
                                  int32_t* pair_slot, int32_t* counts, int32_t* offsets,
                                  int32_t* perm, int32_t* pair_row, uint16_t* x_perm,
                                  int32_t* n_unserved, void* ws, hipStream_t stream,
-                                 const uint8_t* token_valid) {
+                                 const uint8_t* token_valid, void* sched_area) {
   return remap_dispatch(false, ids, T, k, ert, E, R, alive, S, token_valid, nullptr, x, d,
                         pair_slot, counts, offsets, perm, pair_row, x_perm, n_unserved, nullptr,
-                        ws, stream);
+                        ws, stream, sched_area);
 }
 
 hipError_t launch_replay_dispatch(const int32_t* ids, int T, int k, const int32_t* ert, int E,
@@ -613,10 +622,10 @@ hipError_t launch_replay_dispatch(const int32_t* ids, int T, int k, const int32_
                                   const uint16_t* x, int d, int32_t* replay_slot, int32_t* counts,
                                   int32_t* offsets, int32_t* perm, int32_t* replay_row,
                                   uint16_t* x_perm, int32_t* n_unserved, int32_t* n_replayed,
-                                  void* ws, hipStream_t stream) {
+                                  void* ws, hipStream_t stream, void* sched_area) {
   return remap_dispatch(true, ids, T, k, ert, E, R, alive, S, nullptr, prior_slot, x, d,
                         replay_slot, counts, offsets, perm, replay_row, x_perm, n_unserved,
-                        n_replayed, ws, stream);
+                        n_replayed, ws, stream, sched_area);
 }
 
 }  // namespace tg

@@ -51,7 +51,12 @@
 // Tile order: the tiles of one launch are enumerated slot by slot, then by
 // weight panel (n), then by row block (m), so consecutive tiles share a
 // weight panel; each of the 8 XCDs (blocks are dealt to XCDs round robin)
-// takes one contiguous range of that order, keeping a panel in one L2.
+// takes one contiguous range of that order, keeping a panel in one L2. With
+// a schedule area (the fused forward and the replay have one), the first two
+// rounds of each range are dealt statically and the rest are claimed from a
+// per-XCD counter, blocks of an XCD that has run out taking tiles from the
+// other XCDs' counters; the standalone FFN entry point deals every tile
+// statically. Which block runs a tile never changes its bits.
 //
 // Every output element is one fixed sequence of MFMA accumulations over K
 // in increasing order, independent of the row's position, its tile or the
@@ -455,7 +460,8 @@ template <bool SWIGLU, bool GATHER, bool TAIL>
 __global__ __launch_bounds__(256) void grouped_gemm_persistent4_kernel(
     const uint16_t* __restrict__ A, const int32_t* __restrict__ offsets, int S,
     const uint16_t* __restrict__ B, int K, int NW, int I, uint16_t* __restrict__ C, int ldc,
-    int NT, const int32_t* __restrict__ perm, uint32_t kq_magic, int kq_shift, int A_rows) {
+    int NT, const int32_t* __restrict__ perm, uint32_t kq_magic, int kq_shift, int A_rows,
+    int32_t* __restrict__ claims, unsigned long long* __restrict__ slots) {
   constexpr int BM = 256, BN = 256, BK = 64, NWAVE = 4;
   constexpr int CH = BK / 8;                            // 16-byte chunks per staged row
   constexpr int RPI = 64 / CH;                          // staged rows per load instruction
@@ -482,11 +488,69 @@ __global__ __launch_bounds__(256) void grouped_gemm_persistent4_kernel(
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = wave >> 1, wn = wave & 1;
 
+    // Dynamic schedule (claims != nullptr; claims[0..7] are zero at launch).
+    // Rounds 0 and 1 of each XCD's range stay static (tiles lo + c and
+    // lo + P + c); every later tile of XCD x's range is claimed from counter
+    // claims[x], position v giving tile lo_x + 2P + v. A block whose own
+    // range is used up claims from the next XCDs' counters in turn, so that
+    // XCDs that run ahead take work from those behind; every tile is still
+    // run exactly once, and its bits do not depend on where it runs. Lane 0
+    // of wave 0 claims the tile after next when a tile starts and publishes
+    // it after the tile's first stage, as (claim number, tile) in the
+    // block's slot; every wave reads the slot before the tile's last stage
+    // (re-reading until the claim number is the expected one) and uses it at
+    // the next tile switch, so no claim latency lies on the critical path.
+    const bool dyn = claims != nullptr;
+    const int P = per_xcd_blocks;
+    int cl_x = x, cl_v = 0, cl_tries = 0;  // lane 0 of wave 0 only
+    bool cl_done = false;
+    unsigned int cl_seq = 0;               // claims made so far (uniform)
+    auto claim_issue = [&]() {
+      if (tid == 0 && !cl_done) cl_v = atomicAdd(&claims[cl_x], 1);
+    };
+    auto claim_publish = [&]() {
+      if (tid == 0) {
+        int t = -1;
+        while (!cl_done) {
+          const int lx = cl_x * per, hx = min(lx + per, n_head);
+          t = lx + 2 * P + cl_v;
+          if (t < hx) break;
+          t = -1;
+          if (++cl_tries == kXcds) {
+            cl_done = true;
+          } else {
+            cl_x = (cl_x + 1 == kXcds) ? 0 : cl_x + 1;
+            cl_v = atomicAdd(&claims[cl_x], 1);
+          }
+        }
+        __hip_atomic_store(&slots[blockIdx.x],
+                           ((unsigned long long)cl_seq << 32) | (unsigned int)t,
+                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
+    };
+    auto claim_read = [&]() -> int {
+      unsigned long long v;
+      do {
+        v = __hip_atomic_load(&slots[blockIdx.x], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      } while ((unsigned int)(v >> 32) != cl_seq);
+      return __builtin_amdgcn_readfirstlane((int)(unsigned int)v);
+    };
+
     int s_cur = 0, before = 0, pos = 0, c_nt = 0, c_m = 0;
     int o_cur = offsets[0];
     int cnt_cur = offsets[1] - o_cur;
     int mt_cur = (cnt_cur + BM - 1) / BM;
     auto seek = [&](int Lq, int& slot, int& row0, int& rows, int& nt) {
+      if (Lq < pos) {  // a stolen tile before the cursor: walk again from slot 0
+        s_cur = 0;
+        before = 0;
+        pos = 0;
+        c_nt = 0;
+        c_m = 0;
+        o_cur = offsets[0];
+        cnt_cur = offsets[1] - o_cur;
+        mt_cur = (cnt_cur + BM - 1) / BM;
+      }
       while (Lq >= before + mt_cur * NT) {
         before += mt_cur * NT;
         ++s_cur;
@@ -639,6 +703,8 @@ __global__ __launch_bounds__(256) void grouped_gemm_persistent4_kernel(
     a_offsets(row0, rows, a_off);
     int Ln = L + per_xcd_blocks;
     bool has_n = Ln < hi;
+    if (dyn && !has_n) Ln = -1;
+    int nxt2 = -1;  // the tile after next (dynamic schedule)
     int slot_n = slot, row0_n = row0, rows_n = rows, nt_n = nt;
     if (has_n) seek(Ln, slot_n, row0_n, rows_n, nt_n);
     __amdgpu_buffer_rsrc_t a_n = a_of(row0_n, rows_n), b_n = b_of(slot_n, nt_n);
@@ -713,7 +779,11 @@ __global__ __launch_bounds__(256) void grouped_gemm_persistent4_kernel(
     __builtin_amdgcn_sched_barrier(0);                                                     \
   } while (0)
       TG_FRAGS(ab, bb, 0, 0);
-      for (int kt = 0; kt < nk - 1; ++kt) TG_STAGE(kt, false);
+      for (int kt = 0; kt < nk - 1; ++kt) {  // nk >= 2
+        TG_STAGE(kt, false);
+        if (kt == 0 && dyn && has_n) claim_publish();
+      }
+      if (dyn && has_n) nxt2 = claim_read();
       TG_STAGE(nk - 1, true);
 #undef TG_STAGE
       // acc[nb][mb] register r of lane l: row mb*32 + l%32, column
@@ -752,6 +822,10 @@ __global__ __launch_bounds__(256) void grouped_gemm_persistent4_kernel(
     block_barrier();
 
     for (;;) {
+      if (dyn && has_n) {
+        ++cl_seq;
+        claim_issue();
+      }
       if (rows > 128) run_tile(std::integral_constant<int, 0>{});
       else if (rows > 64) run_tile(std::integral_constant<int, 1>{});
       else run_tile(std::integral_constant<int, 2>{});
@@ -763,8 +837,13 @@ __global__ __launch_bounds__(256) void grouped_gemm_persistent4_kernel(
       b_cur = b_n;
 #pragma unroll
       for (int i = 0; i < AI; ++i) a_off[i] = a_off_n[i];
-      Ln += per_xcd_blocks;
-      has_n = Ln < hi;
+      if (dyn) {
+        Ln = nxt2;
+        has_n = Ln >= 0;
+      } else {
+        Ln += per_xcd_blocks;
+        has_n = Ln < hi;
+      }
       if (has_n) {
         seek(Ln, slot_n, row0_n, rows_n, nt_n);
         a_n = a_of(row0_n, rows_n);
@@ -851,13 +930,16 @@ hipError_t launch_grouped(const uint16_t* A, const int32_t* offsets, int S, int 
 template <bool SWIGLU, bool GATHER, bool TAIL>
 hipError_t launch_persistent4(const uint16_t* A, const int32_t* offsets, int S, const uint16_t* B,
                               int K, int NW, int I, uint16_t* C, int ldc, int NT,
-                              hipStream_t stream, const int32_t* perm, int kq, int A_rows) {
+                              hipStream_t stream, const int32_t* perm, int kq, int A_rows,
+                              const GemmSched* sched) {
   int l = 0;
   while ((1 << l) < kq) ++l;
   const uint32_t m = (uint32_t)((((uint64_t)1 << (31 + l)) + (uint64_t)kq - 1) / (uint64_t)kq);
   const int grid = cu_count() / kXcds * kXcds;
+  const bool dyn = sched && sched->claims && grid <= kSchedMaxBlocks;
   hipLaunchKernelGGL((grouped_gemm_persistent4_kernel<SWIGLU, GATHER, TAIL>), dim3(grid), dim3(256),
-                     0, stream, A, offsets, S, B, K, NW, I, C, ldc, NT, perm, m, l, A_rows);
+                     0, stream, A, offsets, S, B, K, NW, I, C, ldc, NT, perm, m, l, A_rows,
+                     dyn ? sched->claims : nullptr, dyn ? sched->slots : nullptr);
   return hipGetLastError();
 }
 
@@ -877,35 +959,37 @@ int panels_down(int d) { return (d + kBN - 1) / kBN; }
 }  // namespace
 
 hipError_t launch_ffn_gateup(const uint16_t* x_perm, const int32_t* offsets, int S, int max_rows,
-                             const uint16_t* w13, int d, int I, uint16_t* h, hipStream_t stream) {
+                             const uint16_t* w13, int d, int I, uint16_t* h, hipStream_t stream,
+                             const GemmSched* sched) {
   if (max_rows == 0) return hipSuccess;
   if (small_batch(S, max_rows))
     return launch_grouped<TG_SMALL, true, false>(x_perm, offsets, S, max_rows, w13, d, 2 * I, I,
                                                  h, I, panels_gateup(I), stream);
   return launch_persistent4<true, false, false>(x_perm, offsets, S, w13, d, 2 * I, I, h, I,
-                                                panels_gateup(I), stream, nullptr, 1, 0);
+                                                panels_gateup(I), stream, nullptr, 1, 0, sched);
 }
 
 hipError_t launch_ffn_gateup_gather(const uint16_t* x, int T, const int32_t* perm, int k,
                                     const int32_t* offsets, int S, int max_rows,
                                     const uint16_t* w13, int d, int I, uint16_t* h,
-                                    hipStream_t stream) {
+                                    hipStream_t stream, const GemmSched* sched) {
   if (max_rows == 0) return hipSuccess;
   if (small_batch(S, max_rows))
     return launch_grouped<TG_SMALL, true, true>(x, offsets, S, max_rows, w13, d, 2 * I, I, h, I,
                                                 panels_gateup(I), stream, perm, k, T);
   return launch_persistent4<true, true, false>(x, offsets, S, w13, d, 2 * I, I, h, I,
-                                               panels_gateup(I), stream, perm, k, T);
+                                               panels_gateup(I), stream, perm, k, T, sched);
 }
 
 hipError_t launch_ffn_down(const uint16_t* h, const int32_t* offsets, int S, int max_rows,
-                           const uint16_t* w2, int d, int I, uint16_t* y, hipStream_t stream) {
+                           const uint16_t* w2, int d, int I, uint16_t* y, hipStream_t stream,
+                           const GemmSched* sched) {
   if (max_rows == 0) return hipSuccess;
   if (small_batch(S, max_rows))
     return launch_grouped<TG_SMALL, false, false>(h, offsets, S, max_rows, w2, I, d, 0, y, d,
                                                   panels_down(d), stream);
   return launch_persistent4<false, false, true>(h, offsets, S, w2, I, d, 0, y, d, panels_down(d),
-                                                stream, nullptr, 1, 0);
+                                                stream, nullptr, 1, 0, sched);
 }
 
 hipError_t launch_expert_ffn(const uint16_t* x_perm, const int32_t* offsets, int S, int max_rows,

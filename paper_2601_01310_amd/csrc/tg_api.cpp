@@ -100,6 +100,7 @@ struct EwLayout {
   uint16_t* x_perm;
   uint16_t* h;
   uint16_t* y;
+  void* sched;
   size_t bytes;
 };
 
@@ -128,6 +129,7 @@ EwLayout ew_layout(const tg_ew_args* a, char* base) {
   L.h = reinterpret_cast<uint16_t*>(take(np * a->I * 2));
   L.y = reinterpret_cast<uint16_t*>(take(a->y ? 0 : np * a->d * 2));
   if (a->y) L.y = a->y;
+  L.sched = take(tg::kSchedBytes);
   L.bytes = off;
   return L;
 }
@@ -145,6 +147,7 @@ struct ReplayLayout {
   uint16_t* x_perm;
   uint16_t* h;
   uint16_t* y2;
+  void* sched;
   size_t bytes;
 };
 
@@ -169,6 +172,7 @@ ReplayLayout replay_layout(const tg_replay_args* a, char* base) {
   L.x_perm = reinterpret_cast<uint16_t*>(take(in_place ? 0 : np * a->d * 2));
   L.h = reinterpret_cast<uint16_t*>(take(np * a->I * 2));
   L.y2 = reinterpret_cast<uint16_t*>(take(np * a->d * 2));
+  L.sched = take(tg::kSchedBytes);
   L.bytes = off;
   return L;
 }
@@ -225,16 +229,19 @@ tg_status ew_forward(const tg_ew_args* a, void* ws, size_t ws_bytes, void* strea
     e = tg::launch_remap_dispatch(ids, a->T, a->k, a->ert, a->E, a->R, a->slot_alive, a->S,
                                   in_place ? nullptr : a->x, a->d, pair_slot, counts, offsets,
                                   L.perm, pair_row, in_place ? nullptr : L.x_perm, n_unserved,
-                                  L.dispatch_ws, s, a->token_valid);
+                                  L.dispatch_ws, s, a->token_valid, L.sched);
   mark(2);
+  // The dispatch has zeroed the GEMMs' dynamic-schedule area.
+  tg::GemmSched sched_gu, sched_dn;
+  tg::sched_carve(L.sched, &sched_gu, &sched_dn);
   if (e == hipSuccess)
     e = in_place ? tg::launch_ffn_gateup_gather(a->x, a->T, L.perm, a->k, offsets, a->S, max_rows,
-                                                a->w13, a->d, a->I, L.h, s)
+                                                a->w13, a->d, a->I, L.h, s, &sched_gu)
                  : tg::launch_ffn_gateup(L.x_perm, offsets, a->S, max_rows, a->w13, a->d, a->I,
-                                         L.h, s);
+                                         L.h, s, &sched_gu);
   mark(3);
   if (e == hipSuccess)
-    e = tg::launch_ffn_down(L.h, offsets, a->S, max_rows, a->w2, a->d, a->I, L.y, s);
+    e = tg::launch_ffn_down(L.h, offsets, a->S, max_rows, a->w2, a->d, a->I, L.y, s, &sched_dn);
   mark(4);
   if (e == hipSuccess) e = tg::launch_combine(L.y, pair_row, w, a->T, a->k, a->d, a->out, s);
   mark(5);
@@ -404,14 +411,17 @@ tg_status tg_ew_replay(const tg_replay_args* a, void* ws, size_t ws_bytes, void*
   hipError_t e = tg::launch_replay_dispatch(
       a->topk_ids, a->T, a->k, a->ert, a->E, a->R, a->slot_alive, a->S, a->pair_slot,
       in_place ? nullptr : a->x, a->d, replay_slot, L.counts, L.offsets, L.perm, L.replay_row,
-      in_place ? nullptr : L.x_perm, n_unserved, n_replayed, L.dispatch_ws, s);
+      in_place ? nullptr : L.x_perm, n_unserved, n_replayed, L.dispatch_ws, s, L.sched);
+  tg::GemmSched sched_gu, sched_dn;
+  tg::sched_carve(L.sched, &sched_gu, &sched_dn);
   if (e == hipSuccess)
     e = in_place ? tg::launch_ffn_gateup_gather(a->x, a->T, L.perm, a->k, L.offsets, a->S,
-                                                max_rows, a->w13, a->d, a->I, L.h, s)
+                                                max_rows, a->w13, a->d, a->I, L.h, s, &sched_gu)
                  : tg::launch_ffn_gateup(L.x_perm, L.offsets, a->S, max_rows, a->w13, a->d, a->I,
-                                         L.h, s);
+                                         L.h, s, &sched_gu);
   if (e == hipSuccess)
-    e = tg::launch_ffn_down(L.h, L.offsets, a->S, max_rows, a->w2, a->d, a->I, L.y2, s);
+    e = tg::launch_ffn_down(L.h, L.offsets, a->S, max_rows, a->w2, a->d, a->I, L.y2, s,
+                            &sched_dn);
   if (e == hipSuccess)
     e = tg::launch_recombine(a->y, a->pair_row, a->pair_slot, a->slot_alive, a->S, L.y2,
                              L.replay_row, a->topk_w, a->T, a->k, a->d, a->out, s);

@@ -19,6 +19,25 @@ tg_status ew_forward(const tg_ew_args* a, void* ws, size_t ws_bytes, void* strea
                      void* const* events);
 tg_status set_error(tg_status s, const char* fmt, ...);
 
+// Work area of the dynamic tile schedule of the two grouped GEMMs of one
+// forward (or replay): per GEMM, 16 claim counters (8 used, one per XCD) and
+// one 8-byte publication slot per block. The dispatch of the same call
+// zeroes the whole area before the GEMMs run.
+constexpr int kSchedMaxBlocks = 1024;
+struct GemmSched {
+  int32_t* claims;
+  unsigned long long* slots;
+};
+constexpr size_t kSchedBytes = 2 * (16 * sizeof(int32_t) + kSchedMaxBlocks * sizeof(unsigned long long));
+// Carves the two GEMMs' schedules out of a kSchedBytes area (base may be null).
+inline void sched_carve(void* base, GemmSched* gateup, GemmSched* down) {
+  char* b = static_cast<char*>(base);
+  gateup->claims = b ? reinterpret_cast<int32_t*>(b) : nullptr;
+  down->claims = b ? reinterpret_cast<int32_t*>(b + 64) : nullptr;
+  gateup->slots = b ? reinterpret_cast<unsigned long long*>(b + 128) : nullptr;
+  down->slots = b ? reinterpret_cast<unsigned long long*>(b + 128 + 8 * kSchedMaxBlocks) : nullptr;
+}
+
 hipError_t launch_gate_topk(const uint16_t* x, const uint16_t* wg, const float* logits_in, int T,
                             int d, int E, int k, float* logits_out, int32_t* ids, float* w,
                             hipStream_t stream);
@@ -36,7 +55,7 @@ hipError_t launch_remap_dispatch(const int32_t* ids, int T, int k, const int32_t
                                  int32_t* pair_slot, int32_t* counts, int32_t* offsets,
                                  int32_t* perm, int32_t* pair_row, uint16_t* x_perm,
                                  int32_t* n_unserved, void* ws, hipStream_t stream,
-                                 const uint8_t* token_valid = nullptr);
+                                 const uint8_t* token_valid = nullptr, void* sched_area = nullptr);
 // Replay batching: pairs whose first-pass slot (prior_slot) is no longer
 // alive, or that had no live candidate, go to their first live candidate now
 // (replay_slot; -1 for every other pair) and are batched by (slot, token,
@@ -47,18 +66,22 @@ hipError_t launch_replay_dispatch(const int32_t* ids, int T, int k, const int32_
                                   const uint16_t* x, int d, int32_t* replay_slot, int32_t* counts,
                                   int32_t* offsets, int32_t* perm, int32_t* replay_row,
                                   uint16_t* x_perm, int32_t* n_unserved, int32_t* n_replayed,
-                                  void* ws, hipStream_t stream);
+                                  void* ws, hipStream_t stream, void* sched_area = nullptr);
 
+// sched (optional): the GEMM's dynamic-schedule area, zeroed before the
+// launch; without it the tiles are dealt statically. Both give the same bits.
 hipError_t launch_ffn_gateup(const uint16_t* x_perm, const int32_t* offsets, int S, int max_rows,
-                             const uint16_t* w13, int d, int I, uint16_t* h, hipStream_t stream);
+                             const uint16_t* w13, int d, int I, uint16_t* h, hipStream_t stream,
+                             const GemmSched* sched = nullptr);
 // Same as launch_ffn_gateup with the activation rows gathered in place:
 // grouped row r is row perm[r] / k of x [T, d] (requires T * d * 2 < 2^31).
 hipError_t launch_ffn_gateup_gather(const uint16_t* x, int T, const int32_t* perm, int k,
                                     const int32_t* offsets, int S, int max_rows,
                                     const uint16_t* w13, int d, int I, uint16_t* h,
-                                    hipStream_t stream);
+                                    hipStream_t stream, const GemmSched* sched = nullptr);
 hipError_t launch_ffn_down(const uint16_t* h, const int32_t* offsets, int S, int max_rows,
-                           const uint16_t* w2, int d, int I, uint16_t* y, hipStream_t stream);
+                           const uint16_t* w2, int d, int I, uint16_t* y, hipStream_t stream,
+                           const GemmSched* sched = nullptr);
 hipError_t launch_expert_ffn(const uint16_t* x_perm, const int32_t* offsets, int S, int max_rows,
                              const uint16_t* w13, const uint16_t* w2, int d, int I, uint16_t* h,
                              uint16_t* y, hipStream_t stream);
