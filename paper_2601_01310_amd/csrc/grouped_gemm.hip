@@ -488,51 +488,93 @@ __global__ __launch_bounds__(256) void grouped_gemm_persistent4_kernel(
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = wave >> 1, wn = wave & 1;
 
-    // Dynamic schedule (claims != nullptr; claims[0..7] are zero at launch).
-    // Rounds 0 and 1 of each XCD's range stay static (tiles lo + c and
-    // lo + P + c); every later tile of XCD x's range is claimed from counter
-    // claims[x], position v giving tile lo_x + 2P + v. A block whose own
-    // range is used up claims from the next XCDs' counters in turn, so that
-    // XCDs that run ahead take work from those behind; every tile is still
-    // run exactly once, and its bits do not depend on where it runs. Lane 0
-    // of wave 0 claims the tile after next when a tile starts and publishes
-    // it after the tile's first stage, as (claim number, tile) in the
-    // block's slot; every wave reads the slot before the tile's last stage
-    // (re-reading until the claim number is the expected one) and uses it at
-    // the next tile switch, so no claim latency lies on the critical path.
+    // Dynamic schedule (claims != nullptr; claims[0..7] and the slots are
+    // zero at launch). Rounds 0-2 of each XCD's range stay static (tiles
+    // lo + c, lo + P + c, lo + 2P + c); every later tile of XCD x's range is
+    // claimed from counter claims[x], position v giving tile lo_x + 3P + v. A
+    // block whose own range is used up claims from the XCD with the most
+    // tiles left, so that XCDs that run ahead take work from those behind;
+    // every tile still runs exactly once, and its bits do not depend on where
+    // it runs. Tile j (j >= 3) of a block is claimed by thread 0 when the
+    // block starts its tile j - 3, published by wave 0 as (j, tile) in slot
+    // j % 2 of the block when that tile ends, loaded by every wave early in
+    // the last stage of tile j - 2 and used at the switch that follows (a
+    // wave that loads the slot before the record lands re-reads it). The
+    // claim and the slot load are plain memory instructions issued by every
+    // thread, with out-of-range offsets where they must do nothing (the
+    // resources are empty without a schedule), and their results are used
+    // only between tiles: no branch or loop makes the compiler wait for them
+    // inside the K loop, so the DMA pipeline never drains for the schedule.
     const bool dyn = claims != nullptr;
     const int P = per_xcd_blocks;
-    int cl_x = x, cl_v = 0, cl_tries = 0;  // lane 0 of wave 0 only
-    bool cl_done = false;
-    unsigned int cl_seq = 0;               // claims made so far (uniform)
+    constexpr int kOut = (int)0x80000000u;  // an offset past any resource: no access
+    constexpr int kCoherent = 16;           // sc1: the device-coherent copy
+    const __amdgpu_buffer_rsrc_t cl_rsrc = make_rsrc(claims, dyn ? kXcds * 4 : 0);
+    const __amdgpu_buffer_rsrc_t sl_rsrc =
+        make_rsrc(dyn ? static_cast<const void*>(slots + 2 * blockIdx.x) : nullptr, dyn ? 16 : 0);
+    auto range_lo = [&](int xx) { return xx * per; };
+    auto range_hi = [&](int xx) { return min(xx * per + per, n_head); };
+    int cl_x = x, cl_v = 0;        // thread 0: the counter claimed from, its last value
+    int cl_last = -1;              // wave 0: the block's latest known tile (-1: none left)
+    unsigned long long slot_v = 0; // the slot as loaded in the last stage of a tile
+    // Read right after the last stage, whose wait has covered both loads, so
+    // that nothing later waits for them: thread 0's claim and the slot.
+    int cl_got = 0, slot_tile = 0, slot_seq = 0;
+    // Tile j + 3's claim, issued when tile j starts (thread 0 only).
     auto claim_issue = [&]() {
-      if (tid == 0 && !cl_done) cl_v = atomicAdd(&claims[cl_x], 1);
+      cl_v = __builtin_amdgcn_raw_ptr_buffer_atomic_add_i32(
+          1, cl_rsrc, (tid == 0 && cl_last >= 0) ? cl_x * 4 : kOut, 0, 0);
     };
-    auto claim_publish = [&]() {
-      if (tid == 0) {
-        int t = -1;
-        while (!cl_done) {
-          const int lx = cl_x * per, hx = min(lx + per, n_head);
-          t = lx + 2 * P + cl_v;
-          if (t < hx) break;
+    // When tile j ends: resolve tile j + 3's claim and publish it (wave 0).
+    auto claim_publish = [&](int jn) {
+      if (wave != 0) return;
+      int t = -1;
+      if (cl_last >= 0) {
+        t = range_lo(cl_x) + 3 * P + cl_got;
+        if (t >= range_hi(cl_x)) {  // this range is used up: take from the fullest one
           t = -1;
-          if (++cl_tries == kXcds) {
-            cl_done = true;
-          } else {
-            cl_x = (cl_x + 1 == kXcds) ? 0 : cl_x + 1;
-            cl_v = atomicAdd(&claims[cl_x], 1);
+          for (int tries = 0; tries < kXcds; ++tries) {
+            const int cv = (int)__builtin_amdgcn_raw_buffer_load_b32(
+                cl_rsrc, lane < kXcds ? lane * 4 : kOut, 0, kCoherent);
+            int left = lane < kXcds ? range_hi(lane) - (range_lo(lane) + 3 * P + cv) : 0;
+            int bx = lane;
+#pragma unroll
+            for (int off = 4; off >= 1; off >>= 1) {
+              const int ol = __shfl_xor(left, off), ox = __shfl_xor(bx, off);
+              if (ol > left || (ol == left && ox < bx)) {
+                left = ol;
+                bx = ox;
+              }
+            }
+            left = __shfl(left, 0);
+            bx = __shfl(bx, 0);
+            if (left <= 0) break;
+            cl_x = bx;
+            const int v = __shfl(__builtin_amdgcn_raw_ptr_buffer_atomic_add_i32(
+                                     1, cl_rsrc, lane == 0 ? cl_x * 4 : kOut, 0, 0),
+                                 0);
+            if (range_lo(cl_x) + 3 * P + v < range_hi(cl_x)) {
+              t = range_lo(cl_x) + 3 * P + v;
+              break;
+            }
           }
         }
-        __hip_atomic_store(&slots[blockIdx.x],
-                           ((unsigned long long)cl_seq << 32) | (unsigned int)t,
-                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       }
+      cl_last = t;
+      typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+      const u32x2 rec = {(unsigned int)t, (unsigned int)jn};
+      __builtin_amdgcn_raw_buffer_store_b64(rec, sl_rsrc, lane == 0 ? (jn & 1) * 8 : kOut, 0,
+                                            kCoherent);
     };
-    auto claim_read = [&]() -> int {
+    // At the switch after tile j - 2: tile j, from the slot loaded in that
+    // tile's last stage.
+    auto claim_result = [&](int jn) -> int {
+      if (slot_seq == jn) return slot_tile;
       unsigned long long v;
-      do {
-        v = __hip_atomic_load(&slots[blockIdx.x], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      } while ((unsigned int)(v >> 32) != cl_seq);
+      do {  // the record had not landed when the slot was read
+        v = __hip_atomic_load(&slots[2 * blockIdx.x + (jn & 1)], __ATOMIC_RELAXED,
+                              __HIP_MEMORY_SCOPE_AGENT);
+      } while ((unsigned int)(v >> 32) != (unsigned int)jn);
       return __builtin_amdgcn_readfirstlane((int)(unsigned int)v);
     };
 
@@ -703,8 +745,11 @@ __global__ __launch_bounds__(256) void grouped_gemm_persistent4_kernel(
     a_offsets(row0, rows, a_off);
     int Ln = L + per_xcd_blocks;
     bool has_n = Ln < hi;
-    if (dyn && !has_n) Ln = -1;
-    int nxt2 = -1;  // the tile after next (dynamic schedule)
+    // The block's tile 2 (static; run only after tile 1).
+    const int t2_static = (has_n && Ln + P < hi) ? Ln + P : -1;
+    if (dyn) cl_last = t2_static;
+    int tj = 0;        // index of the current tile in this block's sequence
+    int slot_off = 0;  // byte offset of the slot read in this tile's last stage: (tj + 2) % 2
     int slot_n = slot, row0_n = row0, rows_n = rows, nt_n = nt;
     if (has_n) seek(Ln, slot_n, row0_n, rows_n, nt_n);
     __amdgpu_buffer_rsrc_t a_n = a_of(row0_n, rows_n), b_n = b_of(slot_n, nt_n);
@@ -745,6 +790,9 @@ __global__ __launch_bounds__(256) void grouped_gemm_persistent4_kernel(
 #define TG_STAGE(kt, LAST)                                                                 \
   do {                                                                                     \
     TG_TARGETS(kt);                                                                        \
+    if constexpr (LAST)                                                                    \
+      slot_v = __builtin_bit_cast(unsigned long long, __builtin_amdgcn_raw_buffer_load_b64(  \
+                                                          sl_rsrc, slot_off, 0, kCoherent)); \
     TG_FRAGS(ab, bb, 1, 1);                                                                \
     TG_ISSUE_A(ra, offa, ka * BK, abn, 0, AI / 2);                                         \
     TG_MFMAS(0, 0, NQ);                                                                    \
@@ -779,12 +827,11 @@ __global__ __launch_bounds__(256) void grouped_gemm_persistent4_kernel(
     __builtin_amdgcn_sched_barrier(0);                                                     \
   } while (0)
       TG_FRAGS(ab, bb, 0, 0);
-      for (int kt = 0; kt < nk - 1; ++kt) {  // nk >= 2
-        TG_STAGE(kt, false);
-        if (kt == 0 && dyn && has_n) claim_publish();
-      }
-      if (dyn && has_n) nxt2 = claim_read();
+      for (int kt = 0; kt < nk - 1; ++kt) TG_STAGE(kt, false);  // nk >= 2
       TG_STAGE(nk - 1, true);
+      cl_got = __builtin_amdgcn_readfirstlane(cl_v);  // thread 0's claim in wave 0
+      slot_tile = __builtin_amdgcn_readfirstlane((int)(unsigned int)slot_v);
+      slot_seq = __builtin_amdgcn_readfirstlane((int)(unsigned int)(slot_v >> 32));
 #undef TG_STAGE
       // acc[nb][mb] register r of lane l: row mb*32 + l%32, column
       // nb*32 + 8*(r/4) + 4*(l/32) + r%4 of the wave's sub-tile; SwiGLU pairs
@@ -822,13 +869,11 @@ __global__ __launch_bounds__(256) void grouped_gemm_persistent4_kernel(
     block_barrier();
 
     for (;;) {
-      if (dyn && has_n) {
-        ++cl_seq;
-        claim_issue();
-      }
+      claim_issue();  // no effect without a schedule or when no tile is left
       if (rows > 128) run_tile(std::integral_constant<int, 0>{});
       else if (rows > 64) run_tile(std::integral_constant<int, 1>{});
       else run_tile(std::integral_constant<int, 2>{});
+      if (dyn) claim_publish(tj + 3);
       if (!has_n) break;
       row0 = row0_n;
       rows = rows_n;
@@ -838,12 +883,14 @@ __global__ __launch_bounds__(256) void grouped_gemm_persistent4_kernel(
 #pragma unroll
       for (int i = 0; i < AI; ++i) a_off[i] = a_off_n[i];
       if (dyn) {
-        Ln = nxt2;
+        Ln = (tj == 0) ? t2_static : claim_result(tj + 2);
         has_n = Ln >= 0;
       } else {
         Ln += per_xcd_blocks;
         has_n = Ln < hi;
       }
+      ++tj;
+      slot_off = (tj & 1) * 8;
       if (has_n) {
         seek(Ln, slot_n, row0_n, rows_n, nt_n);
         a_n = a_of(row0_n, rows_n);
