@@ -156,7 +156,8 @@ def expert_batch_knee(dev, reps=20):
     """Expert FFN latency and throughput against the expert batch size (the
     paper's expert-batch-size knee, App. B), through tg_expert_ffn_grouped with
     all rows in one slot. Slots rotate over 8 copies so the weights come from
-    HBM, not from the 256 MB Infinity Cache."""
+    HBM, not from the 256 MB Infinity Cache. Each size is timed with the
+    launch's own tile choice and with each tile height forced."""
     import torch
 
     from paper_2601_01310_amd import tg
@@ -169,22 +170,31 @@ def expert_batch_knee(dev, reps=20):
         x, w13, w2, h, y = _ffn_buffers(d, I, S, max(Ms), dev)
         for M in Ms:
             offs = [_offsets([M if s == j else 0 for s in range(S)], dev) for j in range(S)]
-            for j in range(3):
-                tg.tg_expert_ffn_grouped(x, offs[j % S], S, M, w13, w2, d, I, h, y)
-            ev = hip.create(2)
-            torch.cuda.synchronize()
-            from ctypes import c_void_p
-            hip.hip.hipEventRecord(c_void_p(ev[0]), c_void_p(torch.cuda.current_stream().cuda_stream))
-            for j in range(reps):
-                tg.tg_expert_ffn_grouped(x, offs[j % S], S, M, w13, w2, d, I, h, y)
-            hip.hip.hipEventRecord(c_void_p(ev[1]), c_void_p(torch.cuda.current_stream().cuda_stream))
-            torch.cuda.synchronize()
-            us = hip.elapsed_ms(ev[0], ev[1]) * 1e3 / reps
-            hip.destroy(ev)
+
+            def timed(policy):
+                from ctypes import c_void_p
+                with tg.tile_policy(policy):
+                    for j in range(3):
+                        tg.tg_expert_ffn_grouped(x, offs[j % S], S, M, w13, w2, d, I, h, y)
+                    ev = hip.create(2)
+                    torch.cuda.synchronize()
+                    stream = c_void_p(torch.cuda.current_stream().cuda_stream)
+                    hip.hip.hipEventRecord(c_void_p(ev[0]), stream)
+                    for j in range(reps):
+                        tg.tg_expert_ffn_grouped(x, offs[j % S], S, M, w13, w2, d, I, h, y)
+                    hip.hip.hipEventRecord(c_void_p(ev[1]), stream)
+                    torch.cuda.synchronize()
+                us = hip.elapsed_ms(ev[0], ev[1]) * 1e3 / reps
+                hip.destroy(ev)
+                return us
+
+            us = timed(tg.TILES_AUTO)
+            us_small, us_full = timed(tg.TILES_SMALL), timed(tg.TILES_FULL)
             flops = 6.0 * d * I * M
             wbytes = 3.0 * d * I * 2
             rec = dict(expert=name, rows=M, us=us, tflops=flops / us / 1e6,
-                       weight_tbps=wbytes / us / 1e6, us_per_row=us / M)
+                       weight_tbps=wbytes / us / 1e6, us_per_row=us / M,
+                       us_32row_tiles=us_small, us_256row_tiles=us_full)
             out.append(rec)
             print(json.dumps(rec), flush=True)
         del x, w13, w2, h, y

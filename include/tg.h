@@ -121,6 +121,27 @@ tg_status tg_expert_ffn_grouped(const uint16_t* x_perm, const int32_t* slot_offs
                                 int d, int I, uint16_t* h, uint16_t* y, void* stream);
 
 /*
+ * Tile height of the grouped expert GEMMs (the FFN of §2.1, in
+ * tg_expert_ffn_grouped, tg_ew_forward and tg_ew_replay), for measurements
+ * and tests; not needed in normal use.
+ *
+ *   TG_TILES_AUTO  (default) each GEMM launch chooses on the device from
+ *                  the slot counts: 32-row tiles for batches whose slots
+ *                  hold few rows (decode steps, a single small expert
+ *                  batch), 256-row tiles otherwise;
+ *   TG_TILES_SMALL every tile 32 rows;
+ *   TG_TILES_FULL  every tile 256 rows (partial last rounds of the down
+ *                  projection still split into 128 x 128 quarters).
+ *
+ * Every choice gives identical bits. The setting is process-wide and read
+ * when a launch is enqueued. Returns TG_ERR_BAD_DIM for any other value.
+ */
+#define TG_TILES_AUTO 0
+#define TG_TILES_SMALL 1
+#define TG_TILES_FULL 2
+tg_status tg_set_gemm_tile_policy(int policy);
+
+/*
  * Gate-weighted combine (§2.1): out[t] = bf16(sum_j topk_w[t,j] * y[pair_row[t,j]])
  * over j = 0..k-1 with pair_row >= 0, float32, in rank order; a token with
  * no routed pair gets +0. On one expert-parallel share this is the share's

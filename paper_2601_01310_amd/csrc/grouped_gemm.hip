@@ -14,39 +14,42 @@
 // consecutive output columns of one row (packed 8-byte epilogue writes).
 //
 // Staging: both tiles go global -> LDS with buffer loads that write LDS
-// directly (no register staging). Activation stages are double-buffered and
-// weight stages triple-buffered (weights are first touched in HBM, so they
-// are requested two stages ahead); at 256 x 256 x 64 this fills the 160 KB
-// of LDS. Each 16-byte chunk sits at an XOR-swizzled position within its
-// row so that fragment reads of consecutive rows hit distinct banks; a lane
-// fetches whichever global chunk the swizzle assigns to its LDS position.
-// The K loop has no branches: each stage ends with one block barrier after
-// which the freed buffers are refilled, and the next stage's first
-// fragments are read while the stage's last MFMAs run. Rows past the end of
-// a group read as zeros through the buffer range check and are never
-// stored; waves whose rows all lie past the end skip their MFMAs. Likewise a
-// slot's last weight panel may be partial (I or d not a multiple of the
-// panel width): its rows past the slot's weights read as zeros and its
-// columns past the output width are never stored.
+// directly (no register staging), in a ring of stage buffers refilled as
+// each stage's closing barrier releases one (weights are first touched in
+// HBM, so they are requested several stages ahead); at 256 x 256 x 64 the
+// stage buffers fill the 160 KB of LDS. Each 16-byte chunk sits at an
+// XOR-swizzled position within its row so that fragment reads of
+// consecutive rows hit distinct banks; a lane fetches whichever global chunk
+// the swizzle assigns to its LDS position. The K loop has no branches: each
+// stage ends with one block barrier after which the freed buffers are
+// refilled, and the next stage's first fragments are read while the stage's
+// last MFMAs run. Rows past the end of a group read as zeros through the
+// buffer range check and are never stored; waves whose rows all lie past the
+// end skip their MFMAs. Likewise a slot's last weight panel may be partial
+// (I or d not a multiple of the panel width): its rows past the slot's
+// weights read as zeros and its columns past the output width are never
+// stored.
 //
 // For GEMM1 the weight tile holds BN/2 gate rows and the matching BN/2 up
 // rows and every wave owns equal numbers of both, so g and u of one output
 // element land in the same lane and register and the SwiGLU epilogue needs
 // no data exchange.
 //
-// Tile shapes: 256 x 256 with 4 waves (one per SIMD, 128 x 128 each) for
-// batches that fill the MFMA units, run by a persistent kernel (one block
-// per CU walking its tiles with the DMA pipeline running on across tiles,
-// results written straight from the accumulators); and 32 x 256 with 4
-// waves (104 KB of LDS), one block per tile, for small per-slot batches,
-// where the launch only streams weights and a 256-row tile would stage and
-// multiply mostly zero rows (results staged through each wave's own LDS
-// region and written as 16-byte row segments). The host picks between the
-// two from the row bound alone (mean rows per slot at most 32), never from
-// the device counts. In the down projection, a partial last round of
-// 256 x 256 tiles that would leave at least half of the CUs idle is run
-// afterwards as 128 x 128 quarter tiles by the same blocks. All shapes give
-// identical bits.
+// Tile shapes: one persistent kernel (one block per CU) runs every launch
+// in one of two shapes, chosen on the device from the slot counts, so that
+// the host never reads them: 256 x 256 tiles with 4 waves (one per SIMD,
+// 128 x 128 each) for batches that fill the MFMA units, walked with the DMA
+// pipeline running on across tiles and results written straight from the
+// accumulators; or 32 x 256 tiles with 4 waves, where a launch mostly
+// streams weights (decode steps, a single small expert batch) and a 256-row
+// tile would stage and multiply mostly zero rows (results staged through
+// each wave's own LDS region and written as 16-byte row segments). The
+// 32-row shape runs when its rounds of tiles over the grid cost less, at
+// about two thirds of a 256-row round each; in the down projection, whose
+// partial last round of 256 x 256 tiles runs as 128 x 128 quarter tiles
+// (keeping the CUs busy with few tiles), only when no slot holds more than
+// 32 rows and the 32-row tiles fill more than one round. All shapes give
+// identical bits, so the choice never changes a result.
 //
 // Tile order: the tiles of one launch are enumerated slot by slot, then by
 // weight panel (n), then by row block (m), so consecutive tiles share a
@@ -55,13 +58,15 @@
 // a schedule area (the fused forward and the replay have one), the first two
 // rounds of each range are dealt statically and the rest are claimed from a
 // per-XCD counter, blocks of an XCD that has run out taking tiles from the
-// other XCDs' counters; the standalone FFN entry point deals every tile
-// statically. Which block runs a tile never changes its bits.
+// other XCDs' counters; the standalone FFN entry point, and 32-row tiles
+// everywhere, deal every tile statically. Which block runs a tile never
+// changes its bits.
 //
 // Every output element is one fixed sequence of MFMA accumulations over K
 // in increasing order, independent of the row's position, its tile or the
 // other rows of its group; a row therefore gives identical bits in any slot
 // holding the same weights (shadow failover, §5.3).
+#include <atomic>
 #include <type_traits>
 
 #include "tg_device.h"
@@ -127,24 +132,33 @@ struct TileInfo {
   int slot, row0, rows, nt;
 };
 
-// Number of tiles of BMx rows x NTx panels over all slots (every lane gets
-// the sum).
-__device__ __forceinline__ int count_tiles(const int32_t* __restrict__ offsets, int S, int BMx,
-                                           int NTx) {
+// Row-block counts of one launch at both tile heights, and its largest slot
+// (every lane gets the results).
+struct Census {
+  int full, small, max_rows;  // 256-row tiles, 32-row tiles (times NTx), largest count
+};
+__device__ __forceinline__ Census census(const int32_t* __restrict__ offsets, int S, int NTx) {
   const int lane = lane_id();
-  int total = 0;
+  int full = 0, small = 0, mx = 0;
   for (int base = 0; base < S; base += kWave) {
     const int s = base + lane;
     const int cnt = (s < S) ? offsets[s + 1] - offsets[s] : 0;
-    int v = (cnt + BMx - 1) / BMx;
+    int f = (cnt + 255) / 256, q = (cnt + 31) / 32, m = cnt;
 #pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off);
-    total += v;
+    for (int off = 32; off >= 1; off >>= 1) {
+      f += __shfl_xor(f, off);
+      q += __shfl_xor(q, off);
+      m = max(m, __shfl_xor(m, off));
+    }
+    full += f;
+    small += q;
+    mx = max(mx, m);
   }
-  return __builtin_amdgcn_readfirstlane(total) * NTx;
+  return {__builtin_amdgcn_readfirstlane(full) * NTx,
+          __builtin_amdgcn_readfirstlane(small) * NTx, __builtin_amdgcn_readfirstlane(mx)};
 }
 
-// Tile L (0 <= L < count_tiles) in the order slot, panel, row block:
+// Tile L of BMx-row tiles in the order slot, panel, row block:
 // its slot, first row, row count, panel and row-block index.
 __device__ __forceinline__ bool find_tile(const int32_t* __restrict__ offsets, int S, int BMx,
                                           int NTx, int L, TileInfo* t, int* m_out) {
@@ -184,35 +198,17 @@ __device__ __forceinline__ bool find_tile(const int32_t* __restrict__ offsets, i
   return false;
 }
 
-// Every wave maps block b to its tile on its own (no LDS, no barrier).
-// Blocks are dealt to the XCDs round robin; block b takes logical tile
-// (b % 8) * (R / 8) + b / 8, so each XCD works through one contiguous range.
-// Returns false (uniformly) when the block has no tile.
-template <int BM>
-__device__ __forceinline__ bool map_tile(const int32_t* __restrict__ offsets, int S, int NT, int b,
-                                         TileInfo* t) {
-  const int total = count_tiles(offsets, S, BM, NT);
-  const int R = (total + kXcds - 1) / kXcds * kXcds;
-  if (b >= R) return false;
-  const int L = (b % kXcds) * (R / kXcds) + b / kXcds;
-  if (L >= total) return false;
-  int m;
-  if (!find_tile(offsets, S, BM, NT, L, t, &m)) return false;
-  const int rows = min(BM, t->rows - m * BM);
-  if (rows <= 0) return false;
-  t->row0 += m * BM;
-  t->rows = rows;
-  return true;
-}
-
-// A (activation) tiles are double-buffered and B (weight) tiles triple-
-// buffered: weight slices are first touched in HBM, so they are requested
-// two stages ahead; activation slices are reused from cache.
+// Both operands stream through one ring of NBUF stage buffers: stage j
+// sits in buffer j % NBUF, and the buffer that stage kt releases at its
+// closing barrier takes stage kt + NBUF, so NBUF - 1 stages are in flight
+// while one is multiplied. A and B of a stage are issued together: the wait
+// for stage kt + 1 (vector loads complete in issue order) then leaves the
+// NBUF - 2 younger stages in flight instead of draining them.
 //
 // GATHER: the activation rows are not pre-permuted; row r of the grouped
 // matrix is row perm[r] / kq of A (the token of routed pair perm[r]), read
 // in place through a buffer resource over all A_rows rows of A.
-template <int BM, int BN, int BK, int WM, int WN, bool SWIGLU, bool GATHER>
+template <int BM, int BN, int BK, int WM, int WN, bool SWIGLU, bool GATHER, int NBUF>
 __device__ __forceinline__ void gemm_tile(uint16_t* smem, const TileInfo& tile,
                                           const uint16_t* __restrict__ A,
                                           const uint16_t* __restrict__ B, int K, int NW, int I,
@@ -230,7 +226,8 @@ __device__ __forceinline__ void gemm_tile(uint16_t* smem, const TileInfo& tile,
   constexpr int WP = WOUT + 8;
   static_assert(MB >= 1 && NB >= 1 && AI >= 1 && BI >= 1 && (BK == 32 || BK == 64), "tile");
   static_assert(!SWIGLU || NB % 2 == 0, "gate/up halves");
-  static_assert(NWAVE * 32 * WP <= 2 * A_ST + 3 * B_ST, "epilogue fits in the stage buffers");
+  static_assert(NBUF >= 2 && (NBUF - 2) * (AI + BI) <= 63, "ring depth within the wait count");
+  static_assert(NWAVE * 32 * WP <= NBUF * (A_ST + B_ST), "epilogue fits in the stage buffers");
 
   const int slot = tile.slot, row0 = tile.row0, rows = tile.rows, nt = tile.nt;
 
@@ -269,7 +266,7 @@ __device__ __forceinline__ void gemm_tile(uint16_t* smem, const TileInfo& tile,
   }
   lds_u16* const smem3 = (lds_u16*)smem;
   const int a_lds = wave * (BM / NWAVE) * BK;
-  const int b_lds = 2 * A_ST + wave * (BN / NWAVE) * BK;
+  const int b_lds = NBUF * A_ST + wave * (BN / NWAVE) * BK;
 #define TG_ISSUE_A(k0, buf)                                                        \
   do {                                                                             \
     _Pragma("unroll") for (int i = 0; i < AI; ++i)                                 \
@@ -291,7 +288,7 @@ __device__ __forceinline__ void gemm_tile(uint16_t* smem, const TileInfo& tile,
 #pragma unroll
   for (int kk = 0; kk < BK / 16; ++kk) {
     xoff[kk] = xrow * BK + (((2 * kk + khalf) ^ swz<CH>(xrow)) << 3);
-    woff[kk] = 2 * A_ST + wrow * BK + (((2 * kk + khalf) ^ swz<CH>(wrow)) << 3);
+    woff[kk] = NBUF * A_ST + wrow * BK + (((2 * kk + khalf) ^ swz<CH>(wrow)) << 3);
   }
   // Weight rows of block nb relative to wrow (gate blocks, then up blocks).
   auto wblk = [](int nb) constexpr {
@@ -327,48 +324,50 @@ __device__ __forceinline__ void gemm_tile(uint16_t* smem, const TileInfo& tile,
                                                     acc[nb][mb], 0, 0, 0);             \
   } while (0)
 
-  // Prologue: A stages 0-1 and B stages 0-2 in flight (indices past the end
-  // re-load the last stage); stage 0 visible; its first fragments loaded.
-  TG_ISSUE_A(0, 0);
-  TG_ISSUE_B(0, 0);
-  TG_ISSUE_B(min(1, nk - 1) * BK, 1);
-  TG_ISSUE_A(min(1, nk - 1) * BK, 1);
-  TG_ISSUE_B(min(2, nk - 1) * BK, 2);
-  TG_WAIT_VM(2 * BI + AI);
+  // Prologue: stages 0 .. NBUF-1 in flight (indices past the end re-load the
+  // last stage, so every wait counts the same loads); stage 0 visible; its
+  // first fragments loaded.
+#pragma unroll
+  for (int j = 0; j < NBUF; ++j) {
+    const int k0 = min(j, nk - 1) * BK;
+    TG_ISSUE_A(k0, j);
+    TG_ISSUE_B(k0, j);
+  }
+  TG_WAIT_VM((NBUF - 1) * (AI + BI));
   block_barrier();
   TG_FRAGS(0, 0, 0, 0);
 
   // Branch-free K loop: every iteration waits, synchronises and refills one
-  // A buffer and one B buffer, so each sub-step is one straight-line region.
-  // A wave whose rows all lie past the group's end (in the tail tile of a
-  // slot) skips the fragment reads and MFMAs but keeps its loads and
-  // barriers.
+  // stage buffer, so each sub-step is one straight-line region. A wave whose
+  // rows all lie past the group's end (in the tail tile of a slot) skips the
+  // fragment reads and MFMAs but keeps its loads and barriers.
   if (wm * (BM / WM) < rows) {
     for (int kt = 0; kt < nk; ++kt) {
-      const int ab = kt & 1, bb = kt % 3;
+      const int cb = kt % NBUF;
 #pragma unroll
       for (int kk = 0; kk < KK - 1; ++kk) {
-        TG_FRAGS(ab, bb, kk + 1, (kk + 1) & 1);
+        TG_FRAGS(cb, cb, kk + 1, (kk + 1) & 1);
         TG_MFMAS(kk & 1);
       }
       // Last sub-step: once every wave holds its fragments of stage kt and
-      // stage kt+1 has landed (only B of stage kt+2 may still be in flight),
-      // stage kt's buffers take A of stage kt+2 and B of stage kt+3, and the
-      // next stage's first fragments are read while the last MFMAs run.
-      TG_WAIT_VM(BI);
+      // stage kt+1 has landed, stage kt's buffer takes stage kt + NBUF, and
+      // the next stage's first fragments are read while the last MFMAs run.
+      TG_WAIT_VM((NBUF - 2) * (AI + BI));
       __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)
       block_barrier();
-      TG_ISSUE_A(min(kt + 2, nk - 1) * BK, ab);
-      TG_ISSUE_B(min(kt + 3, nk - 1) * BK, bb);
-      TG_FRAGS((kt + 1) & 1, (kt + 1) % 3, 0, 0);
+      const int k0 = min(kt + NBUF, nk - 1) * BK;
+      TG_ISSUE_A(k0, cb);
+      TG_ISSUE_B(k0, cb);
+      TG_FRAGS((kt + 1) % NBUF, (kt + 1) % NBUF, 0, 0);
       TG_MFMAS((KK - 1) & 1);
     }
   } else {
     for (int kt = 0; kt < nk; ++kt) {
-      TG_WAIT_VM(BI);
+      TG_WAIT_VM((NBUF - 2) * (AI + BI));
       block_barrier();
-      TG_ISSUE_A(min(kt + 2, nk - 1) * BK, kt & 1);
-      TG_ISSUE_B(min(kt + 3, nk - 1) * BK, kt % 3);
+      const int k0 = min(kt + NBUF, nk - 1) * BK;
+      TG_ISSUE_A(k0, kt % NBUF);
+      TG_ISSUE_B(k0, kt % NBUF);
     }
   }
   TG_WAIT_VM(0);
@@ -460,8 +459,9 @@ template <bool SWIGLU, bool GATHER, bool TAIL>
 __global__ __launch_bounds__(256) void grouped_gemm_persistent4_kernel(
     const uint16_t* __restrict__ A, const int32_t* __restrict__ offsets, int S,
     const uint16_t* __restrict__ B, int K, int NW, int I, uint16_t* __restrict__ C, int ldc,
-    int NT, const int32_t* __restrict__ perm, uint32_t kq_magic, int kq_shift, int A_rows,
-    int32_t* __restrict__ claims, unsigned long long* __restrict__ slots) {
+    int NT, const int32_t* __restrict__ perm, int kq, uint32_t kq_magic, int kq_shift,
+    int A_rows, int32_t* __restrict__ claims, unsigned long long* __restrict__ slots,
+    int policy) {
   constexpr int BM = 256, BN = 256, BK = 64, NWAVE = 4;
   constexpr int CH = BK / 8;                            // 16-byte chunks per staged row
   constexpr int RPI = 64 / CH;                          // staged rows per load instruction
@@ -473,9 +473,38 @@ __global__ __launch_bounds__(256) void grouped_gemm_persistent4_kernel(
   static_assert(!(TAIL && GATHER), "quarter tiles read pre-permuted rows");
   __shared__ __attribute__((aligned(16))) uint16_t smem[2 * A_ST + 3 * B_ST];
 
-  const int total = count_tiles(offsets, S, BM, NT);
   const int per_xcd_blocks = gridDim.x / kXcds;
   const int x = blockIdx.x % kXcds, c = blockIdx.x / kXcds;
+  const int G = gridDim.x;
+  const Census cs = census(offsets, S, NT);
+  bool small_tiles = policy == kTilesSmall;
+  if (policy == kTilesAuto) {
+    // Rounds of tiles over the grid at each height; a 32-row round costs
+    // about two thirds of a 256-row round (it streams the same weight panel
+    // with an eighth of the MFMA work). With the quarter split of a partial
+    // last round (TAIL) the 256-row walk keeps the CUs busy even with few
+    // tiles; there 32-row tiles pay only when no slot exceeds 32 rows and
+    // they fill more than one round.
+    const int rs = (cs.small + G - 1) / G, rf = (cs.full + G - 1) / G;
+    small_tiles = TAIL ? (cs.max_rows <= 32 && cs.small > G) : 2 * rs < 3 * rf;
+  }
+  if (small_tiles) {
+    // 32 x 256 tiles, each XCD walking one contiguous range of them.
+    const int per_s = (cs.small + kXcds - 1) / kXcds;
+    const int hi_s = min(x * per_s + per_s, cs.small);
+    for (int q = x * per_s + c; q < hi_s; q += per_xcd_blocks) {
+      TileInfo t;
+      int m;
+      if (!find_tile(offsets, S, 32, NT, q, &t, &m)) break;
+      t.row0 += m * 32;
+      t.rows = min(32, t.rows - m * 32);
+      gemm_tile<32, BN, BK, 1, 4, SWIGLU, GATHER, 4>(smem, t, A, B, K, NW, I, C, ldc, perm, kq,
+                                                    A_rows);
+      __syncthreads();
+    }
+    return;
+  }
+  const int total = cs.full;
   const int rem = TAIL ? total % (int)gridDim.x : 0;
   const bool tail = rem > 0 && 2 * rem <= (int)gridDim.x;
   const int n_head = tail ? total - rem : total;
@@ -726,16 +755,18 @@ __global__ __launch_bounds__(256) void grouped_gemm_persistent4_kernel(
 
     // A of stage kt+1 and B of stage kt+2 go into the buffers released at
     // the previous barrier: this tile's, else the next tile's, else (no next
-    // tile) this tile's last stage again.
-#define TG_TARGETS(kt)                                                                     \
-  const bool ca = (kt) + 1 < nk, cb = (kt) + 2 < nk;                                       \
-  const int ka = ca ? (kt) + 1 : (has_n ? (kt) + 1 - nk : nk - 1);                         \
+    // tile) this tile's last stage again. Without a next tile its operands
+    // (a_n, b_n, a_off_n) are the current tile's, so a load past the end of
+    // this tile may always take them. A of stage kt+1 lies in this tile in
+    // every stage but the last (LAST, known to the compiler).
+#define TG_TARGETS(kt, LAST)                                                               \
+  const bool cb = (kt) + 2 < nk;                                                           \
+  const int ka = !(LAST) ? (kt) + 1 : (has_n ? 0 : nk - 1);                                \
   const int kb = cb ? (kt) + 2 : (has_n ? (kt) + 2 - nk : nk - 1);                         \
-  const bool a_here = ca || !has_n;                                                        \
-  const __amdgpu_buffer_rsrc_t ra = a_here ? a_cur : a_n;                                  \
-  const __amdgpu_buffer_rsrc_t rb = (cb || !has_n) ? b_cur : b_n;                          \
+  const __amdgpu_buffer_rsrc_t ra = !(LAST) ? a_cur : a_n;                                 \
+  const __amdgpu_buffer_rsrc_t rb = cb ? b_cur : b_n;                                      \
   int offa[AI];                                                                            \
-  _Pragma("unroll") for (int i = 0; i < AI; ++i) offa[i] = a_here ? a_off[i] : a_off_n[i]; \
+  _Pragma("unroll") for (int i = 0; i < AI; ++i) offa[i] = !(LAST) ? a_off[i] : a_off_n[i]; \
   const int abn = ab ^ 1, bbn = (bb == 0) ? 2 : bb - 1
 
     int slot, row0, rows, nt;
@@ -789,12 +820,12 @@ __global__ __launch_bounds__(256) void grouped_gemm_persistent4_kernel(
       // barrier (the next tile may run in another mode).
 #define TG_STAGE(kt, LAST)                                                                 \
   do {                                                                                     \
-    TG_TARGETS(kt);                                                                        \
+    TG_TARGETS(kt, LAST);                                                                        \
     if constexpr (LAST)                                                                    \
       slot_v = __builtin_bit_cast(unsigned long long, __builtin_amdgcn_raw_buffer_load_b64(  \
                                                           sl_rsrc, slot_off, 0, kCoherent)); \
     TG_FRAGS(ab, bb, 1, 1);                                                                \
-    TG_ISSUE_A(ra, offa, ka * BK, abn, 0, AI / 2);                                         \
+    TG_ISSUE_A(ra, offa, ka * BK, abn, 0, AI / 2);                                        \
     TG_MFMAS(0, 0, NQ);                                                                    \
     TG_PATTERN_LOADS;                                                                      \
     __builtin_amdgcn_sched_barrier(0);                                                     \
@@ -928,25 +959,12 @@ __global__ __launch_bounds__(256) void grouped_gemm_persistent4_kernel(
       if (rows > 0 && col0 < ldc) {
         t.row0 += m * (BM / 2);
         t.rows = rows;
-        gemm_tile<BM / 2, BN / 2, BK, 2, 2, SWIGLU, GATHER>(smem, t, A, B, K, NW, I, C, ldc, perm, 1,
-                                                         A_rows);
+        gemm_tile<BM / 2, BN / 2, BK, 2, 2, SWIGLU, GATHER, 4>(smem, t, A, B, K, NW, I, C, ldc,
+                                                            perm, 1, A_rows);
         __syncthreads();
       }
     }
   }
-}
-
-// One block per tile (the small-batch shape).
-template <int BM, int BN, int BK, int WM, int WN, bool SWIGLU, bool GATHER>
-__global__ __launch_bounds__(64 * WM * WN) void grouped_gemm_kernel(
-    const uint16_t* __restrict__ A, const int32_t* __restrict__ offsets, int S,
-    const uint16_t* __restrict__ B, int K, int NW, int I, uint16_t* __restrict__ C, int ldc,
-    int NT, const int32_t* __restrict__ perm, int kq, int A_rows) {
-  __shared__ __attribute__((aligned(16))) uint16_t smem[2 * BM * BK + 3 * BN * BK];
-  TileInfo tile;
-  if (map_tile<BM>(offsets, S, NT, blockIdx.x, &tile))
-    gemm_tile<BM, BN, BK, WM, WN, SWIGLU, GATHER>(smem, tile, A, B, K, NW, I, C, ldc, perm, kq,
-                                                  A_rows);
 }
 
 int cu_count() {
@@ -957,20 +975,7 @@ int cu_count() {
   return n;
 }
 
-template <int BM, int BN, int BK, int WM, int WN, bool SWIGLU, bool GATHER>
-hipError_t launch_grouped(const uint16_t* A, const int32_t* offsets, int S, int max_rows,
-                          const uint16_t* B, int K, int NW, int I, uint16_t* C, int ldc, int NT,
-                          hipStream_t stream, const int32_t* perm = nullptr, int kq = 1,
-                          int A_rows = 0) {
-  // Bound on the tile count: sum_s ceil(count_s / BM) <= ceil(max_rows / BM) + S.
-  const long bound = ((long)(max_rows + BM - 1) / BM + S) * NT;
-  const long grid = (bound + kXcds - 1) / kXcds * kXcds;
-  if (grid == 0) return hipSuccess;
-  hipLaunchKernelGGL((grouped_gemm_kernel<BM, BN, BK, WM, WN, SWIGLU, GATHER>),
-                     dim3((unsigned)grid), dim3(64 * WM * WN), 0, stream, A, offsets, S, B, K, NW,
-                     I, C, ldc, NT, perm, kq, A_rows);
-  return hipGetLastError();
-}
+std::atomic<int> g_tile_policy{kTilesAuto};
 
 // Launch of the 4-wave persistent kernel: one block per CU (a multiple of
 // 8); K of at least 2 stages (d and I are multiples of 64, at least 128).
@@ -985,16 +990,13 @@ hipError_t launch_persistent4(const uint16_t* A, const int32_t* offsets, int S, 
   const int grid = cu_count() / kXcds * kXcds;
   const bool dyn = sched && sched->claims && grid <= kSchedMaxBlocks;
   hipLaunchKernelGGL((grouped_gemm_persistent4_kernel<SWIGLU, GATHER, TAIL>), dim3(grid), dim3(256),
-                     0, stream, A, offsets, S, B, K, NW, I, C, ldc, NT, perm, m, l, A_rows,
-                     dyn ? sched->claims : nullptr, dyn ? sched->slots : nullptr);
+                     0, stream, A, offsets, S, B, K, NW, I, C, ldc, NT, perm, kq, m, l, A_rows,
+                     dyn ? sched->claims : nullptr, dyn ? sched->slots : nullptr,
+                     g_tile_policy.load(std::memory_order_relaxed));
   return hipGetLastError();
 }
 
-#define TG_SMALL 32, 256, 64, 1, 4
 constexpr int kBN = 256;
-constexpr int kSmallRowsPerSlot = 32;
-
-bool small_batch(int S, int max_rows) { return max_rows <= kSmallRowsPerSlot * (long)S; }
 
 // Weight panels per slot: gate/up panels hold kBN / 2 output columns (as
 // many gate as up rows), down panels kBN. A last, partial panel (I or d not
@@ -1005,13 +1007,12 @@ int panels_down(int d) { return (d + kBN - 1) / kBN; }
 
 }  // namespace
 
+void set_tile_policy(int policy) { g_tile_policy.store(policy, std::memory_order_relaxed); }
+
 hipError_t launch_ffn_gateup(const uint16_t* x_perm, const int32_t* offsets, int S, int max_rows,
                              const uint16_t* w13, int d, int I, uint16_t* h, hipStream_t stream,
                              const GemmSched* sched) {
   if (max_rows == 0) return hipSuccess;
-  if (small_batch(S, max_rows))
-    return launch_grouped<TG_SMALL, true, false>(x_perm, offsets, S, max_rows, w13, d, 2 * I, I,
-                                                 h, I, panels_gateup(I), stream);
   return launch_persistent4<true, false, false>(x_perm, offsets, S, w13, d, 2 * I, I, h, I,
                                                 panels_gateup(I), stream, nullptr, 1, 0, sched);
 }
@@ -1021,9 +1022,6 @@ hipError_t launch_ffn_gateup_gather(const uint16_t* x, int T, const int32_t* per
                                     const uint16_t* w13, int d, int I, uint16_t* h,
                                     hipStream_t stream, const GemmSched* sched) {
   if (max_rows == 0) return hipSuccess;
-  if (small_batch(S, max_rows))
-    return launch_grouped<TG_SMALL, true, true>(x, offsets, S, max_rows, w13, d, 2 * I, I, h, I,
-                                                panels_gateup(I), stream, perm, k, T);
   return launch_persistent4<true, true, false>(x, offsets, S, w13, d, 2 * I, I, h, I,
                                                panels_gateup(I), stream, perm, k, T, sched);
 }
@@ -1032,9 +1030,6 @@ hipError_t launch_ffn_down(const uint16_t* h, const int32_t* offsets, int S, int
                            const uint16_t* w2, int d, int I, uint16_t* y, hipStream_t stream,
                            const GemmSched* sched) {
   if (max_rows == 0) return hipSuccess;
-  if (small_batch(S, max_rows))
-    return launch_grouped<TG_SMALL, false, false>(h, offsets, S, max_rows, w2, I, d, 0, y, d,
-                                                  panels_down(d), stream);
   return launch_persistent4<false, false, true>(h, offsets, S, w2, I, d, 0, y, d, panels_down(d),
                                                 stream, nullptr, 1, 0, sched);
 }

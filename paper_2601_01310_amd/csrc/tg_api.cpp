@@ -346,6 +346,13 @@ tg_status tg_expert_ffn_grouped(const uint16_t* x_perm, const int32_t* slot_offs
                     "tg_expert_ffn_grouped");
 }
 
+tg_status tg_set_gemm_tile_policy(int policy) {
+  if (policy != TG_TILES_AUTO && policy != TG_TILES_SMALL && policy != TG_TILES_FULL)
+    return fail(TG_ERR_BAD_DIM, "tile policy %d is not one of 0, 1, 2", policy);
+  tg::set_tile_policy(policy);
+  return TG_OK;
+}
+
 tg_status tg_combine(const uint16_t* y, const int32_t* pair_row, const float* topk_w, int T, int k,
                      int d, uint16_t* out, void* stream) {
   tg_status st;

@@ -69,6 +69,11 @@ hipError_t launch_replay_dispatch(const int32_t* ids, int T, int k, const int32_
                                   uint16_t* x_perm, int32_t* n_unserved, int32_t* n_replayed,
                                   void* ws, hipStream_t stream, void* sched_area = nullptr);
 
+// Tile height of the grouped GEMMs: chosen per launch on the device (auto)
+// or forced; every choice gives the same bits.
+enum TilePolicy { kTilesAuto = 0, kTilesSmall = 1, kTilesFull = 2 };
+void set_tile_policy(int policy);
+
 // sched (optional): the GEMM's dynamic-schedule area, zeroed before the
 // launch; without it the tiles are dealt statically. Both give the same bits.
 hipError_t launch_ffn_gateup(const uint16_t* x_perm, const int32_t* offsets, int S, int max_rows,

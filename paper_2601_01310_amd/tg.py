@@ -20,7 +20,7 @@ TG_OK, TG_ERR_NULL_ARG, TG_ERR_BAD_DIM, TG_ERR_UNSUPPORTED, TG_ERR_WORKSPACE, TG
 
 EXPORTS = [
     "tg_status_string", "tg_last_error", "tg_gate_topk", "tg_remap_dispatch_workspace",
-    "tg_remap_dispatch", "tg_expert_ffn_grouped", "tg_combine", "tg_ew_forward_workspace",
+    "tg_remap_dispatch", "tg_expert_ffn_grouped", "tg_set_gemm_tile_policy", "tg_combine", "tg_ew_forward_workspace",
     "tg_ew_forward", "tg_ew_forward_timed", "tg_ew_forward_noalloc", "tg_ew_replay_workspace", "tg_ew_replay",
     "tg_batch_trigger", "tg_kv_checkpoint", "tg_kv_checkpoint_strided", "tg_kv_restore",
 ]
@@ -77,6 +77,8 @@ def load(path: Optional[str] = None):
                                       vp, sz, vp]
     lib.tg_expert_ffn_grouped.restype = i
     lib.tg_expert_ffn_grouped.argtypes = [vp, vp, i, i, vp, vp, i, i, vp, vp, vp]
+    lib.tg_set_gemm_tile_policy.argtypes = [i]
+    lib.tg_set_gemm_tile_policy.restype = i
     lib.tg_combine.restype = i
     lib.tg_combine.argtypes = [vp, vp, vp, i, i, i, vp, vp]
     lib.tg_ew_forward_workspace.restype = sz
@@ -153,6 +155,27 @@ def tg_expert_ffn_grouped(x_perm, slot_offsets, S, max_rows, w13, w2, d, I, h, y
     _check(load().tg_expert_ffn_grouped(_p(x_perm), _p(slot_offsets), S, max_rows, _p(w13), _p(w2),
                                         d, I, _p(h), _p(y), _stream(stream)),
            "tg_expert_ffn_grouped")
+
+
+TILES_AUTO, TILES_SMALL, TILES_FULL = 0, 1, 2
+
+
+def tg_set_gemm_tile_policy(policy):
+    _check(load().tg_set_gemm_tile_policy(policy), "tg_set_gemm_tile_policy")
+
+
+class tile_policy:
+    """Context manager: the grouped GEMMs' tile height forced for a block."""
+
+    def __init__(self, policy):
+        self.policy = policy
+
+    def __enter__(self):
+        tg_set_gemm_tile_policy(self.policy)
+        return self
+
+    def __exit__(self, *exc):
+        tg_set_gemm_tile_policy(TILES_AUTO)
 
 
 def tg_combine(y, pair_row, topk_w, T, k, d, out, stream=None):

@@ -95,31 +95,37 @@ def test_ffn_entry_point_rows_independent_of_position(tiny):
 
 
 def test_ffn_tile_shapes_give_identical_bits(tiny):
-    """The row bound selects the tile shape (32-row tiles when it allows at
-    most 32 rows per slot on average, else 256-row tiles); both shapes give
+    """32-row and 256-row tiles (forced, and the launch's own choice) give
     the same bits on the same rows, across full tiles and ragged tails."""
     d, I, S = tiny.d, tiny.I, tiny.S
     cnt = torch.tensor([0, 33, 1, 70, 0, 64, 31, 40, 29, 32], dtype=torch.int32)
     assert cnt.numel() == S
-    P = int(cnt.sum())                     # 300 <= 32 * S: small tiles at max_rows = P
-    big = 32 * S + 1                       # large tiles
+    P = int(cnt.sum())
     g = torch.Generator().manual_seed(7)
-    x_perm = torch.randn((big, d), generator=g).to(torch.bfloat16).to(DEV)
+    x_perm = torch.randn((P, d), generator=g).to(torch.bfloat16).to(DEV)
     offsets = torch.zeros(S + 1, dtype=torch.int32)
     offsets[1:] = torch.cumsum(cnt, 0)
     offsets = offsets.to(DEV)
     outs = []
-    for max_rows in (P, big):
-        h = torch.zeros((big, I), dtype=torch.bfloat16, device=DEV)
-        y = torch.zeros((big, d), dtype=torch.bfloat16, device=DEV)
-        tg.tg_expert_ffn_grouped(x_perm, offsets, S, max_rows, tiny.w13, tiny.w2, d, I, h, y)
+    for policy in (tg.TILES_SMALL, tg.TILES_FULL, tg.TILES_AUTO):
+        h = torch.zeros((P, I), dtype=torch.bfloat16, device=DEV)
+        y = torch.zeros((P, d), dtype=torch.bfloat16, device=DEV)
+        with tg.tile_policy(policy):
+            tg.tg_expert_ffn_grouped(x_perm, offsets, S, P, tiny.w13, tiny.w2, d, I, h, y)
         torch.cuda.synchronize()
-        outs.append((u16(h[:P]), u16(y[:P])))
-    assert np.array_equal(outs[0][0], outs[1][0]), "h differs between tile shapes"
-    assert np.array_equal(outs[0][1], outs[1][1]), "y differs between tile shapes"
+        outs.append((u16(h), u16(y)))
+    for o in outs[1:]:
+        assert np.array_equal(outs[0][0], o[0]), "h differs between tile shapes"
+        assert np.array_equal(outs[0][1], o[1]), "y differs between tile shapes"
     o = int(offsets[3])
     ref = O.expert_ffn(u16(x_perm[o:o + 70]), u16(tiny.w13[3]), u16(tiny.w2[3]))[1]
     G.assert_close_bf16(outs[0][1][o:o + 70], ref, "y slot 3")
+
+
+def test_tile_policy_rejects_unknown_values():
+    with pytest.raises(tg.TgError):
+        tg.tg_set_gemm_tile_policy(3)
+    tg.tg_set_gemm_tile_policy(tg.TILES_AUTO)
 
 
 @pytest.mark.parametrize("big", [700, 1700], ids=["spill16", "spill80"])
@@ -158,37 +164,69 @@ def test_ffn_partial_last_round_split_matches_oracle(big):
 
 def test_persistent_walk_matches_small_tiles_bitwise():
     """Forty slots, every other one empty, with row counts around the tile
-    edges (1, 31, 32, 33, 255, 256, 257, ...): with max_rows at most 32 per
-    slot the 32-row kernel runs, one block per tile; above it the persistent
-    kernel walks 320 gate/up tiles over the CUs (more than one per block,
-    across the empty slots) and runs all of the down GEMM's tiles as tail
-    quarters. Both must give the same bits, and the oracle's values."""
+    edges (1, 31, 32, 33, 255, 256, 257, ...). With 256-row tiles the
+    persistent walk runs 320 gate/up tiles over the CUs (more than one per
+    block, across the empty slots) and all of the down GEMM's tiles as tail
+    quarters; with 32-row tiles each block walks its range of those. Both,
+    and the launch's own choice, give the same bits and the oracle's
+    values."""
     d, I, S = 1024, 2560, 40
     base = [0, 1, 31, 32, 33, 255, 256, 257, 0, 0, 2, 63, 64, 65, 100, 0, 17, 5, 1, 0]
     counts = [c for b in base for c in (b, 0)]
     P = sum(counts)
-    assert len(counts) == S and P <= 32 * S
+    assert len(counts) == S
     assert sum((c + 255) // 256 for c in counts) * (2 * I // 256) == 320
-    big = 32 * S + 1
     g = torch.Generator().manual_seed(21)
-    x = torch.randn((big, d), generator=g).to(torch.bfloat16).to(DEV)
+    x = torch.randn((P, d), generator=g).to(torch.bfloat16).to(DEV)
     w13 = (torch.randn((S, 2 * I, d), generator=g) * 0.02).to(torch.bfloat16).to(DEV)
     w2 = (torch.randn((S, d, I), generator=g) * 0.02).to(torch.bfloat16).to(DEV)
     off = np.concatenate([[0], np.cumsum(counts)]).astype(np.int32)
     offd = torch.from_numpy(off).to(DEV)
     res = []
-    for max_rows in (P, big):
-        h = torch.zeros((big, I), dtype=torch.bfloat16, device=DEV)
-        y = torch.zeros((big, d), dtype=torch.bfloat16, device=DEV)
-        tg.tg_expert_ffn_grouped(x, offd, S, max_rows, w13, w2, d, I, h, y)
+    for policy in (tg.TILES_SMALL, tg.TILES_FULL, tg.TILES_AUTO):
+        h = torch.zeros((P, I), dtype=torch.bfloat16, device=DEV)
+        y = torch.zeros((P, d), dtype=torch.bfloat16, device=DEV)
+        with tg.tile_policy(policy):
+            tg.tg_expert_ffn_grouped(x, offd, S, P, w13, w2, d, I, h, y)
         torch.cuda.synchronize()
-        res.append((u16(h[:P]), u16(y[:P])))
-    assert np.array_equal(res[0][0], res[1][0]), "h: persistent vs 32-row tiles"
-    assert np.array_equal(res[0][1], res[1][1]), "y: persistent vs 32-row tiles"
+        res.append((u16(h), u16(y)))
+    for r in res[1:]:
+        assert np.array_equal(res[0][0], r[0]), "h: 256-row vs 32-row tiles"
+        assert np.array_equal(res[0][1], r[1]), "y: 256-row vs 32-row tiles"
     for s_ in (10, 12, 14, 28):
         a, b = int(off[s_]), int(off[s_ + 1])
         ref = O.expert_ffn(u16(x[a:b]), u16(w13[s_]), u16(w2[s_]))[1]
         G.assert_close_bf16(res[1][1][a:b], ref, f"y slot {s_}")
+
+
+@pytest.mark.parametrize("name", ["dsv3_decode", "mixtral_small"])
+def test_fused_forward_tile_policies_give_identical_bits(name):
+    """The fused forward (gathered rows read in place) under each tile
+    height: 32-row tiles everywhere, 256-row tiles everywhere and the
+    launch's own choice give the same per-pair outputs and outputs, which
+    match the oracle on every row."""
+    if name == "mixtral_small":
+        wl = synth.make_custom(T=96, d=4096, E=8, k=2, I=14336, n_local=8, shadow_experts=[2],
+                               gate="weights", seed=5, device=DEV)
+    else:
+        wl = synth.make(name, device=DEV)
+    print(f"[gpu] tile policies on {name}", flush=True)
+    res = []
+    for policy in (tg.TILES_SMALL, tg.TILES_FULL, tg.TILES_AUTO):
+        with tg.tile_policy(policy):
+            f = tg.EwForward(wl, keep_y=True)
+            f()
+            torch.cuda.synchronize()
+        P = int(f.slot_offsets[-1])
+        res.append((u16(f.y[:P]), u16(f.out), host(f.pair_row)))
+        del f
+    for r in res[1:]:
+        assert np.array_equal(res[0][2], r[2])
+        assert np.array_equal(res[0][0], r[0]), "y differs between tile policies"
+        assert np.array_equal(res[0][1], r[1]), "out differs between tile policies"
+    ref = _oracle_full(wl)
+    G.assert_close_bf16(res[2][0], ref["y"], "y (every row)")
+    G.assert_out_close(res[2][1], ref, "out (every token)")
 
 
 def test_repeat_calls_are_bit_identical(tiny):
