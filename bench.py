@@ -28,22 +28,24 @@ RIDGE_FLOP_PER_BYTE = PEAK_BF16_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9)
 STAGES = ["gate", "dispatch", "ffn_gateup", "ffn_down", "combine"]
 GEMM_SRC = [os.path.join(ROOT, "paper_2601_01310_amd", "csrc", f)
             for f in ("grouped_gemm.hip", "tg_device.h")]
-TRAFFIC = os.path.join(ROOT, "profiles", "gemm_gateup_mixtral_traffic.json")
+TRAFFIC = os.path.join(ROOT, "profiles", "gemm_traffic.json")
 
 
 def measured_traffic(workload: str):
-    """HBM-side bytes per dispatch of the gate/up GEMM from the committed
-    rocprofv3 FETCH_SIZE / WRITE_SIZE runs, or None when they were taken on
-    another workload or before the kernel source last changed."""
+    """HBM-side bytes per dispatch of the gate/up GEMM on this workload from
+    the committed rocprofv3 FETCH_SIZE / WRITE_SIZE runs, or None when they
+    were not taken on it or were taken before the kernel source last
+    changed."""
     import hashlib
     try:
         rec = json.load(open(TRAFFIC))
     except (OSError, ValueError):
         return None
     sha = hashlib.sha256(b"".join(open(f, "rb").read() for f in GEMM_SRC)).hexdigest()
-    if rec.get("source_sha256") != sha or rec.get("workload") != workload:
+    w = rec.get("workloads", {}).get(workload)
+    if rec.get("source_sha256") != sha or not w:
         return None
-    return rec.get("traffic_bytes_per_dispatch")
+    return w["gateup"]["traffic_bytes_per_dispatch"]
 
 
 class HipEvents:
@@ -627,7 +629,7 @@ def compact(wl, r):
            "pairs_per_s": r["pairs_per_s"], "step_ms_p50": r["step_ms_p50"],
            "ms_per_step": r["ms_per_step"],
            "stages_ms": {k: round(v, 4) for k, v in r["stages_ms"].items()},
-           "roofline": r["roofline"]}
+           "roofline": dict(r["roofline"], traffic=measured_traffic(wl.name))}
     if r["roofline"]["bound"] == "hbm":
         out["step_hbm_frac"] = r["step_hbm_frac"]
     else:
@@ -646,6 +648,8 @@ def main():
     ap.add_argument("--failover", action="store_true",
                     help="time the run with the workload's failed primaries rerouted to shadows")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-failover", action="store_true",
+                    help="skip the interleaved healthy / rerouted blocks (profiling runs)")
     ap.add_argument("--no-others", action="store_true",
                     help="time only the named workload (by default the mixtral line also carries "
                          "the DeepSeek-V3 share, skewed and decode workloads under 'workloads')")
@@ -705,7 +709,8 @@ def main():
         checkpoint_cost(wl, args.steps, args.warmup)
         return
     alive = wl.alive_after_failure() if args.failover else wl.alive
-    res = measure_workload(wl, alive, args.steps, args.warmup, with_failover=not args.failover)
+    res = measure_workload(wl, alive, args.steps, args.warmup,
+                           with_failover=not (args.failover or args.no_failover))
     P, touched, stage_ms = res["routed_pairs"], res["touched_slots"], res["stages_ms"]
     d, I = wl.d, wl.I
     line = {
