@@ -401,6 +401,67 @@ def test_batch_trigger_brute_force_over_delivery_and_liveness():
             assert cond == (0 if everyone else 1 if rows >= min_rows else 2)
 
 
+def test_batch_trigger_agrees_with_the_arrival_process():
+    """§5.2 as a process in time: AWs deliver their chunks one after another
+    (seeded random order, some never), failure detection can mark AWs
+    unhealthy at any moment, and the EW starts at the first moment when
+    every AW still healthy has delivered, or else when the rows buffered
+    from healthy AWs reach the minimum, or else when the probe window ends.
+    At each event before that moment the snapshot rule must say "not yet"
+    (condition 2 with the window still open); at the starting moment it must
+    give the reason the process started for (all delivered has priority over
+    the minimum when both happen at the same event), and the batch must hold
+    exactly the rows delivered so far by healthy AWs."""
+    rng = np.random.default_rng(77)
+    for trial in range(400):
+        A = int(rng.integers(1, 7))
+        sizes = rng.integers(0, 30, A)
+        chunk_rows = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int64)
+        T = int(chunk_rows[-1] + rng.integers(-10, 5))
+        T = max(T, 0)
+        rows_in = [min(max(int(chunk_rows[a + 1]), 0), T) - min(max(int(chunk_rows[a]), 0), T)
+                   for a in range(A)]
+        min_rows = int(rng.integers(0, max(2, sum(rows_in) + 5)))
+        # events: ("d", a) a delivery, ("f", a) a failure detection; some AWs never deliver
+        events = [("d", a) for a in range(A) if rng.random() < 0.8]
+        events += [("f", a) for a in range(A) if rng.random() < 0.25]
+        rng.shuffle(events)
+        window = int(rng.integers(0, len(events) + 2))  # the probe window ends after this many events
+        delivered = np.zeros(A, np.uint8)
+        alive = np.ones(A, np.uint8)
+        started = None
+        for i in range(len(events) + 1):
+            if i > 0:
+                kind, a = events[i - 1]
+                if kind == "d":
+                    delivered[a] = 1
+                else:
+                    alive[a] = 0
+            healthy = [a for a in range(A) if alive[a]]
+            everyone = all(delivered[a] for a in healthy)
+            have = sum(rows_in[a] for a in healthy if delivered[a])
+            reason = 0 if everyone else 1 if have >= min_rows else None
+            if reason is None and i >= window:
+                reason = 2
+            cond, tv, rows, n = O.batch_trigger(delivered, alive, chunk_rows, T, min_rows)
+            if reason is None:
+                assert cond == 2, (trial, i)
+                continue
+            started = (reason, cond, tv, rows, n, delivered.copy(), alive.copy())
+            break
+        if started is None:  # every event seen, window still open: the EW waits on
+            continue
+        reason, cond, tv, rows, n, dl, al = started
+        assert cond == reason, (trial, reason, cond)
+        want = np.zeros(T, np.uint8)
+        for a in range(A):
+            if dl[a] and al[a]:
+                lo, hi = min(max(int(chunk_rows[a]), 0), T), min(max(int(chunk_rows[a + 1]), 0), T)
+                want[lo:hi] = 1
+        assert np.array_equal(tv, want) and rows == int(want.sum())
+        assert n == int(sum(1 for a in range(A) if dl[a] and al[a]))
+
+
 # ---------------------------------------------------------------- replay (§5.1)
 
 
