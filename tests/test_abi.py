@@ -46,6 +46,14 @@ def test_status_strings(lib):
     assert lib.tg_status_string(99) == b"TG_ERR_UNKNOWN"
 
 
+def test_tile_policy_accepts_the_three_settings_only(lib):
+    for bad in (-1, 3, 1 << 20):
+        assert lib.tg_set_gemm_tile_policy(bad) == tg.TG_ERR_BAD_DIM
+    assert b"tile policy" in lib.tg_last_error()
+    for good in (tg.TILES_SMALL, tg.TILES_FULL, tg.TILES_AUTO):  # ends on the default
+        assert lib.tg_set_gemm_tile_policy(good) == tg.TG_OK
+
+
 def _gate(lib, **kw):
     a = dict(x=P, w_gate=P, logits_in=None, T=4, d=256, E=8, k=2, logits_out=None, ids=P, w=P)
     a.update(kw)
