@@ -15,8 +15,9 @@
  *   - All tensor pointers are DEVICE pointers to dense row-major arrays.
  *     bf16 values travel as uint16_t bit patterns.
  *   - The caller owns every buffer; the library allocates nothing and keeps
- *     no state between calls. (The one exception, tg_ew_forward_noalloc,
- *     takes its workspace from a scratch area the library holds per GPU.)
+ *     no state between calls. (The exceptions: tg_ew_forward_noalloc takes
+ *     its workspace from a scratch area the library holds per GPU, and
+ *     tg_set_gemm_tile_policy sets a process-wide measurement knob.)
  *   - Work is enqueued on `stream` (a hipStream_t; NULL = default stream)
  *     and is asynchronous: no call synchronises with the host. Data-dependent
  *     sizes (per-slot counts) stay on the device.

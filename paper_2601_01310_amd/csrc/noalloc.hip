@@ -8,8 +8,11 @@
 // on holds its own copy, at its own address, until the process ends; the
 // host-side name `scratch` is only a stand-in, so host code uses the device
 // address resolved once per device with hipGetSymbolAddress, never the name.
-// Nothing in the forward's workspace has to start at zero (every kernel
-// writes what a later kernel reads), so the area is never cleared.
+// Nothing in the forward's workspace has to start at zero when the call is
+// made: every kernel writes what a later kernel reads, and what must be zero
+// when a kernel starts (the grouped GEMMs' tile counters and claim slots) is
+// cleared by the forward's own dispatch kernels, so the host never clears
+// the area.
 #include <hip/hip_runtime.h>
 
 #include <atomic>
