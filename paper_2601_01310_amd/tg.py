@@ -20,9 +20,10 @@ TG_OK, TG_ERR_NULL_ARG, TG_ERR_BAD_DIM, TG_ERR_UNSUPPORTED, TG_ERR_WORKSPACE, TG
 
 EXPORTS = [
     "tg_status_string", "tg_last_error", "tg_gate_topk", "tg_remap_dispatch_workspace",
-    "tg_remap_dispatch", "tg_expert_ffn_grouped", "tg_set_gemm_tile_policy", "tg_combine", "tg_ew_forward_workspace",
-    "tg_ew_forward", "tg_ew_forward_timed", "tg_ew_forward_noalloc", "tg_ew_replay_workspace", "tg_ew_replay",
-    "tg_batch_trigger", "tg_kv_checkpoint", "tg_kv_checkpoint_strided", "tg_kv_restore",
+    "tg_remap_dispatch", "tg_expert_ffn_grouped", "tg_set_gemm_tile_policy", "tg_combine",
+    "tg_ew_forward_workspace", "tg_ew_forward", "tg_ew_forward_timed", "tg_ew_forward_noalloc",
+    "tg_ew_replay_workspace", "tg_ew_replay", "tg_batch_trigger", "tg_kv_checkpoint",
+    "tg_kv_checkpoint_strided", "tg_kv_restore",
 ]
 
 
