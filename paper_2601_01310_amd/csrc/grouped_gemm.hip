@@ -517,7 +517,7 @@ __global__ __launch_bounds__(256) void grouped_gemm_persistent4_kernel(
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = wave >> 1, wn = wave & 1;
 
-    // Dynamic schedule (claims != nullptr; claims[0..7] and the slots are
+    // Dynamic schedule (claims != nullptr; claims[0..8] and the slots are
     // zero at launch). Rounds 0-2 of each XCD's range stay static (tiles
     // lo + c, lo + P + c, lo + 2P + c); every later tile of XCD x's range is
     // claimed from counter claims[x], position v giving tile lo_x + 3P + v. A
@@ -944,23 +944,51 @@ __global__ __launch_bounds__(256) void grouped_gemm_persistent4_kernel(
   if constexpr (TAIL) {
     if (!tail) return;
     __syncthreads();
-    const int nq = 4 * rem;
-    const int qper = (nq + kXcds - 1) / kXcds;
-    const int qhi = min(x * qper + qper, nq);
-    for (int q = x * qper + c; q < qhi; q += per_xcd_blocks) {
+    // The spilled tiles run as 128-column halves of their upper and lower
+    // 128 rows: pieces 0 .. 2 rem - 1 are the upper halves of every spilled
+    // tile (two column halves each), pieces 2 rem .. 4 rem - 1 the lower
+    // halves, which are empty for tiles of at most 128 rows. With a schedule
+    // area the pieces are claimed from a counter (claims[8]), so that blocks
+    // whose walk held cheap partial tiles, and end it early, take more of
+    // them; without one they are dealt round robin over the grid. Each piece
+    // runs at the height its rows need, with as many stage buffers as that
+    // height leaves room for in LDS: with a long K a piece is bound by the
+    // latency of its weight stream, not by its MFMAs.
+    const int npieces = 4 * rem;
+    int* const piece_ctr = claims ? claims + kXcds : nullptr;
+    // Thread 0 claims the next piece; the block reads it through LDS, whose
+    // stage buffers are free between pieces.
+    auto next_piece = [&](int prev) {
+      if (!piece_ctr) return prev < 0 ? (int)blockIdx.x : prev + G;
+      __syncthreads();
+      if (threadIdx.x == 0) reinterpret_cast<int*>(smem)[0] = atomicAdd(piece_ctr, 1);
+      __syncthreads();
+      const int v = reinterpret_cast<const int*>(smem)[0];
+      __syncthreads();  // every wave has read it before the next piece's loads land
+      return v;
+    };
+    for (int p = next_piece(-1); p < npieces; p = next_piece(p)) {
+      const int half = p / (2 * rem), r = p - half * (2 * rem);
       TileInfo t;
       int m;
-      if (!find_tile(offsets, S, BM, NT, n_head + q / 4, &t, &m)) break;
-      m = 2 * m + (q % 4) / 2;
-      t.nt = 2 * t.nt + q % 2;
+      if (!find_tile(offsets, S, BM, NT, n_head + r / 2, &t, &m)) break;
+      m = 2 * m + half;
+      t.nt = 2 * t.nt + (r & 1);
       const int rows = min(BM / 2, t.rows - m * (BM / 2));
-      // A quarter past a partial last panel has no output column to store.
+      // A piece past a partial last panel has no output column to store.
       const int col0 = t.nt * (SWIGLU ? BN / 4 : BN / 2);
       if (rows > 0 && col0 < ldc) {
         t.row0 += m * (BM / 2);
         t.rows = rows;
-        gemm_tile<BM / 2, BN / 2, BK, 2, 2, SWIGLU, GATHER, 4>(smem, t, A, B, K, NW, I, C, ldc,
-                                                            perm, 1, A_rows);
+        if (rows <= 32)
+          gemm_tile<32, BN / 2, BK, 1, 4, SWIGLU, GATHER, 8>(smem, t, A, B, K, NW, I, C, ldc, perm,
+                                                            1, A_rows);
+        else if (rows <= 64)
+          gemm_tile<64, BN / 2, BK, 2, 2, SWIGLU, GATHER, 6>(smem, t, A, B, K, NW, I, C, ldc, perm,
+                                                            1, A_rows);
+        else
+          gemm_tile<BM / 2, BN / 2, BK, 2, 2, SWIGLU, GATHER, 5>(smem, t, A, B, K, NW, I, C, ldc,
+                                                              perm, 1, A_rows);
         __syncthreads();
       }
     }

@@ -20,8 +20,9 @@ tg_status ew_forward(const tg_ew_args* a, void* ws, size_t ws_bytes, void* strea
 tg_status set_error(tg_status s, const char* fmt, ...);
 
 // Work area of the dynamic tile schedule of the two grouped GEMMs of one
-// forward (or replay): per GEMM, 16 claim counters (8 used, one per XCD) and
-// two 8-byte publication slots per block. The dispatch of the same call
+// forward (or replay): per GEMM, 16 claim counters (one per XCD for the
+// tile walk, then one for the pieces of a spilled last round; the rest
+// unused) and two 8-byte publication slots per block. The dispatch of the same call
 // zeroes the whole area before the GEMMs run.
 constexpr int kSchedMaxBlocks = 1024;
 struct GemmSched {
