@@ -31,17 +31,32 @@ GEMM_SRC = [os.path.join(ROOT, "paper_2601_01310_amd", "csrc", f)
 TRAFFIC = os.path.join(ROOT, "profiles", "gemm_traffic.json")
 
 
+def kernel_source_hash(paths) -> str:
+    """sha256 of the kernel sources with comments and blank lines removed:
+    it changes when the code changes, not when a comment does."""
+    import hashlib
+    import re
+    out = []
+    for f in paths:
+        text = open(f, encoding="utf-8").read()
+        text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+        for line in text.splitlines():
+            line = re.sub(r"//.*", "", line).rstrip()
+            if line.strip():
+                out.append(line)
+    return hashlib.sha256("\n".join(out).encode()).hexdigest()
+
+
 def measured_traffic(workload: str):
     """HBM-side bytes per dispatch of the gate/up GEMM on this workload from
     the committed rocprofv3 FETCH_SIZE / WRITE_SIZE runs, or None when they
     were not taken on it or were taken before the kernel source last
     changed."""
-    import hashlib
     try:
         rec = json.load(open(TRAFFIC))
     except (OSError, ValueError):
         return None
-    sha = hashlib.sha256(b"".join(open(f, "rb").read() for f in GEMM_SRC)).hexdigest()
+    sha = kernel_source_hash(GEMM_SRC)
     w = rec.get("workloads", {}).get(workload)
     if rec.get("source_sha256") != sha or not w:
         return None

@@ -55,12 +55,13 @@
 // weight panel (n), then by row block (m), so consecutive tiles share a
 // weight panel; each of the 8 XCDs (blocks are dealt to XCDs round robin)
 // takes one contiguous range of that order, keeping a panel in one L2. With
-// a schedule area (the fused forward and the replay have one), the first two
-// rounds of each range are dealt statically and the rest are claimed from a
-// per-XCD counter, blocks of an XCD that has run out taking tiles from the
-// other XCDs' counters; the standalone FFN entry point, and 32-row tiles
-// everywhere, deal every tile statically. Which block runs a tile never
-// changes its bits.
+// a schedule area (the fused forward and the replay have one), the first
+// three rounds of each range are dealt statically and the rest are claimed
+// from a per-XCD counter, blocks of an XCD that has run out taking tiles
+// from the other XCDs' counters, and the pieces of a spilled last round are
+// claimed from one more counter; the standalone FFN entry point, and 32-row
+// tiles everywhere, deal every tile statically. Which block runs a tile
+// never changes its bits.
 //
 // Every output element is one fixed sequence of MFMA accumulations over K
 // in increasing order, independent of the row's position, its tile or the

@@ -36,3 +36,13 @@ def test_quantiles_and_compact_summary():
          "roofline": {"bound": "hbm", "frac": 0.76}, "step_hbm_frac": 0.72, "step_flop_frac": 0.0}
     c = bench.compact(wl, r)
     assert c["step_hbm_frac"] == 0.72 and "step_flop_frac" not in c and "failover" not in c
+
+
+def test_kernel_source_hash_ignores_comments_but_not_code(tmp_path):
+    a = tmp_path / "a.hip"
+    a.write_text("// header\nint f(int x) {\n  return x + 1;  // add one\n}\n/* block\n comment */\n")
+    h0 = bench.kernel_source_hash([str(a)])
+    a.write_text("// another header\n\nint f(int x) {\n  return x + 1;\n}\n")
+    assert bench.kernel_source_hash([str(a)]) == h0
+    a.write_text("int f(int x) {\n  return x + 2;\n}\n")
+    assert bench.kernel_source_hash([str(a)]) != h0
