@@ -162,6 +162,49 @@ def test_ffn_partial_last_round_split_matches_oracle(big):
     assert np.array_equal(Y[:n], ys[1][1]), "rows differ between layouts with and without a spill"
 
 
+@pytest.mark.parametrize("tail", [20, 50, 100])
+def test_down_spill_in_the_forward_matches_the_standalone_ffn_and_oracle(tail):
+    """The down projection's spilled last round, claimed from a counter in
+    the fused forward and dealt statically by the standalone FFN entry
+    point: 8 slots of 1024 rows and one of 1024 + tail rows give 37 row
+    blocks of 16 column panels (d = 4096), two full rounds of 256 tiles and
+    a spill of the last slot's 80 tiles. Its full row blocks run as 128-row
+    quarters and its tail as 32-, 64- or 128-row pieces (tail = 20, 50,
+    100). Routing is exact (one-hot logits, top-1); the two entry points give
+    the same bits, and every row matches the oracle."""
+    d, I, E = 4096, 128, 9
+    counts = [1024] * 8 + [1024 + tail]
+    T = sum(counts)
+    print(f"[gpu] down spill, tail {tail}: T={T}", flush=True)
+    wl = synth.make_custom(T=T, d=d, E=E, k=1, I=I, n_local=E, shadow_experts=[], gate="logits",
+                           seed=61 + tail, device=DEV)
+    rng = np.random.default_rng(tail)
+    assign = rng.permutation(np.repeat(np.arange(E), counts))
+    logits = torch.zeros((T, E), dtype=torch.float32)
+    logits[torch.arange(T), torch.from_numpy(assign)] = 8.0
+    wl.logits = logits.to(DEV)
+    f = tg.EwForward(wl, keep_y=True)
+    f()
+    torch.cuda.synchronize()
+    assert np.array_equal(host(f.slot_counts), np.array(counts))
+    rows = host(f.pair_row)[:, 0]
+    y_fwd = u16(f.y[:T])
+    # the same rows in slot order through the standalone entry point
+    x_perm = torch.empty_like(wl.x)
+    x_perm[torch.from_numpy(rows).long().to(DEV)] = wl.x
+    h = torch.empty((T, I), dtype=torch.bfloat16, device=DEV)
+    y = torch.empty((T, d), dtype=torch.bfloat16, device=DEV)
+    tg.tg_expert_ffn_grouped(x_perm, f.slot_offsets, wl.S, T, wl.w13, wl.w2, d, I, h, y)
+    torch.cuda.synchronize()
+    assert np.array_equal(u16(y), y_fwd), "forward (claimed spill) vs standalone (static spill)"
+    off = host(f.slot_offsets)
+    xp = u16(x_perm)
+    for s_ in range(E):
+        a, b = int(off[s_]), int(off[s_ + 1])
+        ref = O.expert_ffn(xp[a:b], u16(wl.w13[s_]), u16(wl.w2[s_]))[1]
+        G.assert_close_bf16(y_fwd[a:b], ref, f"y slot {s_}")
+
+
 def test_persistent_walk_matches_small_tiles_bitwise():
     """Forty slots, every other one empty, with row counts around the tile
     edges (1, 31, 32, 33, 255, 256, 257, ...). With 256-row tiles the
