@@ -205,6 +205,36 @@ def test_down_spill_in_the_forward_matches_the_standalone_ffn_and_oracle(tail):
         G.assert_close_bf16(y_fwd[a:b], ref, f"y slot {s_}")
 
 
+@pytest.mark.parametrize("extra", [0, 1], ids=["half_round_spilled", "one_more_not_spilled"])
+def test_down_spill_threshold_edges_match_oracle(extra):
+    """The down projection spills its partial last round when that round
+    fills at most half of the grid. With one column panel (d = 256) and full
+    row blocks, a last round of exactly half the grid is spilled and one of
+    half the grid plus one tile is not; every row matches the oracle on both
+    sides of the edge."""
+    grid = torch.cuda.get_device_properties(0).multi_processor_count // 8 * 8
+    d, I, S = 256, 128, 3
+    print(f"[gpu] spill edge, grid {grid}, extra {extra}", flush=True)
+    blocks = grid + grid // 2 + extra               # tiles of the down GEMM (one panel)
+    split = [blocks // 3, blocks // 3, blocks - 2 * (blocks // 3)]
+    counts = [256 * b for b in split]
+    g = torch.Generator().manual_seed(71)
+    P = sum(counts)
+    x = torch.randn((P, d), generator=g).to(torch.bfloat16).to(DEV)
+    w13 = (torch.randn((S, 2 * I, d), generator=g) * 0.05).to(torch.bfloat16).to(DEV)
+    w2 = (torch.randn((S, d, I), generator=g) * 0.05).to(torch.bfloat16).to(DEV)
+    off = np.concatenate([[0], np.cumsum(counts)]).astype(np.int32)
+    h = torch.empty((P, I), dtype=torch.bfloat16, device=DEV)
+    y = torch.empty((P, d), dtype=torch.bfloat16, device=DEV)
+    tg.tg_expert_ffn_grouped(x, torch.from_numpy(off).to(DEV), S, P, w13, w2, d, I, h, y)
+    torch.cuda.synchronize()
+    Y = u16(y)
+    for s_ in range(S):
+        a, b = int(off[s_]), int(off[s_ + 1])
+        ref = O.expert_ffn(u16(x[a:b]), u16(w13[s_]), u16(w2[s_]))[1]
+        G.assert_close_bf16(Y[a:b], ref, f"y slot {s_} (grid {grid}, extra {extra})")
+
+
 def test_persistent_walk_matches_small_tiles_bitwise():
     """Forty slots, every other one empty, with row counts around the tile
     edges (1, 31, 32, 33, 255, 256, 257, ...). With 256-row tiles the
