@@ -221,3 +221,22 @@ def test_binding_refuses_host_tensors(lib):
     import torch
     with pytest.raises(ValueError):
         tg.tg_combine(torch.zeros(4), None, None, 1, 1, 256, None, stream=0)
+
+
+def test_readme_c_example_compiles_against_the_header(tmp_path):
+    """The C function in README.md is valid C against include/tg.h."""
+    import re
+    import shutil
+    import subprocess
+    cc = shutil.which("gcc") or shutil.which("cc")
+    if cc is None:
+        pytest.skip("no C compiler")
+    text = open(os.path.join(ROOT, "README.md")).read()
+    blocks = re.findall(r"```c\n(.*?)```", text, flags=re.S)
+    assert blocks, "README.md has no C example"
+    src = tmp_path / "example.c"
+    src.write_text(blocks[0])
+    r = subprocess.run([cc, "-std=c11", "-Wall", "-Werror", "-fsyntax-only",
+                        f"-I{os.path.join(ROOT, 'include')}", str(src)],
+                       capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
