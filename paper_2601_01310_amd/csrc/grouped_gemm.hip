@@ -67,6 +67,7 @@
 // in increasing order, independent of the row's position, its tile or the
 // other rows of its group; a row therefore gives identical bits in any slot
 // holding the same weights (shadow failover, §5.3).
+#include <algorithm>
 #include <atomic>
 #include <type_traits>
 
@@ -1016,7 +1017,7 @@ hipError_t launch_persistent4(const uint16_t* A, const int32_t* offsets, int S, 
   int l = 0;
   while ((1 << l) < kq) ++l;
   const uint32_t m = (uint32_t)((((uint64_t)1 << (31 + l)) + (uint64_t)kq - 1) / (uint64_t)kq);
-  const int grid = cu_count() / kXcds * kXcds;
+  const int grid = std::max(kXcds, cu_count() / kXcds * kXcds);  // a multiple of 8, never 0
   const bool dyn = sched && sched->claims && grid <= kSchedMaxBlocks;
   hipLaunchKernelGGL((grouped_gemm_persistent4_kernel<SWIGLU, GATHER, TAIL>), dim3(grid), dim3(256),
                      0, stream, A, offsets, S, B, K, NW, I, C, ldc, NT, perm, kq, m, l, A_rows,
