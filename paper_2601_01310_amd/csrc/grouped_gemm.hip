@@ -55,9 +55,9 @@
 // weight panel (n), then by row block (m), so consecutive tiles share a
 // weight panel; each of the 8 XCDs (blocks are dealt to XCDs round robin)
 // takes one contiguous range of that order, keeping a panel in one L2. With
-// a schedule area (the fused forward and the replay have one), the first
-// three rounds of each range are dealt statically and the rest are claimed
-// from a per-XCD counter, blocks of an XCD that has run out taking tiles
+// a schedule area (the fused forward and the replay have one), all but the
+// last three rounds of each range (at least three) are dealt statically and
+// the rest are claimed from a per-XCD counter, blocks of an XCD that has run out taking tiles
 // from the other XCDs' counters, and the pieces of a spilled last round are
 // claimed from one more counter; the standalone FFN entry point, and 32-row
 // tiles everywhere, deal every tile statically. Which block runs a tile
@@ -78,6 +78,7 @@ namespace tg {
 namespace {
 
 constexpr int kXcds = 8;
+constexpr int kDynRounds = 3;  // last rounds of each XCD's range that are claimed, not dealt
 
 // XOR swizzle of the 16-byte chunks of a staged row (CH chunks per row);
 // fragment reads of 8 or 16 consecutive rows hit distinct banks.
@@ -520,17 +521,22 @@ __global__ __launch_bounds__(256) void grouped_gemm_persistent4_kernel(
     const int wm = wave >> 1, wn = wave & 1;
 
     // Dynamic schedule (claims != nullptr; claims[0..8] and the slots are
-    // zero at launch). Rounds 0-2 of each XCD's range stay static (tiles
-    // lo + c, lo + P + c, lo + 2P + c); every later tile of XCD x's range is
-    // claimed from counter claims[x], position v giving tile lo_x + 3P + v. A
+    // zero at launch). The first R rounds of each XCD's range are dealt
+    // statically (tile lo + jP + c is the block's tile j), R being all but
+    // the last three rounds and at least 3: blocks that start the same round
+    // together stream the same weight panels close together in time, so
+    // they share them in L2. Every later tile of XCD x's range is claimed
+    // from counter claims[x], position v giving tile lo_x + RP + v. A
     // block whose own range is used up claims from the XCD with the most
     // tiles left, so that XCDs that run ahead take work from those behind;
     // every tile still runs exactly once, and its bits do not depend on where
     // it runs. Tile j (j >= 3) of a block is claimed by thread 0 when the
-    // block starts its tile j - 3, published by wave 0 as (j, tile) in slot
-    // j % 2 of the block when that tile ends, loaded by every wave early in
-    // the last stage of tile j - 2 and used at the switch that follows (a
-    // wave that loads the slot before the record lands re-reads it). The
+    // block starts its tile j - 3 (a static tile needs no claim; a block
+    // whose static tiles pass its range's end claims instead), published by
+    // wave 0 as (j, tile) in slot j % 2 of the block when that tile ends,
+    // loaded by every wave early in the last stage of tile j - 2 and used at
+    // the switch that follows (a wave that loads the slot before the record
+    // lands re-reads it). The
     // claim and the slot load are plain memory instructions issued by every
     // thread, with out-of-range offsets where they must do nothing (the
     // resources are empty without a schedule), and their results are used
@@ -552,22 +558,26 @@ __global__ __launch_bounds__(256) void grouped_gemm_persistent4_kernel(
     // that nothing later waits for them: thread 0's claim and the slot.
     int cl_got = 0, slot_tile = 0, slot_seq = 0;
     // Tile j + 3's claim, issued when tile j starts (thread 0 only).
-    auto claim_issue = [&]() {
+    const int R = max(3, (per + P - 1) / P - kDynRounds);  // static rounds
+    auto static_tile = [&](int j) { return j < R && lo + j * P + c < hi; };
+    auto claim_issue = [&](int j) {
       cl_v = __builtin_amdgcn_raw_ptr_buffer_atomic_add_i32(
-          1, cl_rsrc, (tid == 0 && cl_last >= 0) ? cl_x * 4 : kOut, 0, 0);
+          1, cl_rsrc, (tid == 0 && cl_last >= 0 && !static_tile(j + 3)) ? cl_x * 4 : kOut, 0, 0);
     };
     // When tile j ends: resolve tile j + 3's claim and publish it (wave 0).
     auto claim_publish = [&](int jn) {
       if (wave != 0) return;
       int t = -1;
-      if (cl_last >= 0) {
-        t = range_lo(cl_x) + 3 * P + cl_got;
+      if (cl_last >= 0 && static_tile(jn)) {
+        t = lo + jn * P + c;
+      } else if (cl_last >= 0) {
+        t = range_lo(cl_x) + R * P + cl_got;
         if (t >= range_hi(cl_x)) {  // this range is used up: take from the fullest one
           t = -1;
           for (int tries = 0; tries < kXcds; ++tries) {
             const int cv = (int)__builtin_amdgcn_raw_buffer_load_b32(
                 cl_rsrc, lane < kXcds ? lane * 4 : kOut, 0, kCoherent);
-            int left = lane < kXcds ? range_hi(lane) - (range_lo(lane) + 3 * P + cv) : 0;
+            int left = lane < kXcds ? range_hi(lane) - (range_lo(lane) + R * P + cv) : 0;
             int bx = lane;
 #pragma unroll
             for (int off = 4; off >= 1; off >>= 1) {
@@ -584,8 +594,8 @@ __global__ __launch_bounds__(256) void grouped_gemm_persistent4_kernel(
             const int v = __shfl(__builtin_amdgcn_raw_ptr_buffer_atomic_add_i32(
                                      1, cl_rsrc, lane == 0 ? cl_x * 4 : kOut, 0, 0),
                                  0);
-            if (range_lo(cl_x) + 3 * P + v < range_hi(cl_x)) {
-              t = range_lo(cl_x) + 3 * P + v;
+            if (range_lo(cl_x) + R * P + v < range_hi(cl_x)) {
+              t = range_lo(cl_x) + R * P + v;
               break;
             }
           }
@@ -902,7 +912,7 @@ __global__ __launch_bounds__(256) void grouped_gemm_persistent4_kernel(
     block_barrier();
 
     for (;;) {
-      claim_issue();  // no effect without a schedule or when no tile is left
+      claim_issue(tj);  // no effect without a schedule or when no tile is left
       if (rows > 128) run_tile(std::integral_constant<int, 0>{});
       else if (rows > 64) run_tile(std::integral_constant<int, 1>{});
       else run_tile(std::integral_constant<int, 2>{});
