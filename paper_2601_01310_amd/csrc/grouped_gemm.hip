@@ -492,17 +492,28 @@ __global__ __launch_bounds__(256) void grouped_gemm_persistent4_kernel(
     small_tiles = TAIL ? (cs.max_rows <= 32 && cs.small > G) : 2 * rs < 3 * rf;
   }
   if (small_tiles) {
-    // 32 x 256 tiles, each XCD walking one contiguous range of them.
-    const int per_s = (cs.small + kXcds - 1) / kXcds;
-    const int hi_s = min(x * per_s + per_s, cs.small);
+    // 32 x 256 tiles (gate/up) or 32 x 128 tiles (down), each XCD walking
+    // one contiguous range of them. These launches stream weights; the down
+    // projection's narrower tiles split its panels finely enough to even out
+    // the blocks' shares (32 slots of d = 7168: 1792 tiles, 7 per block,
+    // instead of 896, 3 or 4 per block), and their smaller stages leave room
+    // for a deeper ring.
+    constexpr int NS = SWIGLU ? 1 : 2;  // tiles per 256-column panel
+    const int n_small = cs.small * NS;
+    const int per_s = (n_small + kXcds - 1) / kXcds;
+    const int hi_s = min(x * per_s + per_s, n_small);
     for (int q = x * per_s + c; q < hi_s; q += per_xcd_blocks) {
       TileInfo t;
       int m;
-      if (!find_tile(offsets, S, 32, NT, q, &t, &m)) break;
+      if (!find_tile(offsets, S, 32, NT * NS, q, &t, &m)) break;
       t.row0 += m * 32;
       t.rows = min(32, t.rows - m * 32);
-      gemm_tile<32, BN, BK, 1, 4, SWIGLU, GATHER, 4>(smem, t, A, B, K, NW, I, C, ldc, perm, kq,
-                                                    A_rows);
+      if constexpr (SWIGLU)
+        gemm_tile<32, BN, BK, 1, 4, SWIGLU, GATHER, 4>(smem, t, A, B, K, NW, I, C, ldc, perm, kq,
+                                                      A_rows);
+      else
+        gemm_tile<32, BN / 2, BK, 1, 4, SWIGLU, GATHER, 8>(smem, t, A, B, K, NW, I, C, ldc, perm,
+                                                          kq, A_rows);
       __syncthreads();
     }
     return;
