@@ -205,6 +205,48 @@ def test_down_spill_in_the_forward_matches_the_standalone_ffn_and_oracle(tail):
         G.assert_close_bf16(y_fwd[a:b], ref, f"y slot {s_}")
 
 
+def test_gateup_walk_with_claimed_last_rounds_matches_the_standalone_ffn_and_oracle():
+    """With more than six rounds of tiles per XCD, the fused forward deals
+    all but the last three statically and claims the rest from counters; the
+    standalone FFN entry point deals every tile statically. 8 slots of 610 to
+    701 rows (three row blocks each, the last one partial, so the blocks
+    drift apart) times 128 gate/up panels (I = 16384, d = 256) give 3072
+    tiles, twelve rounds on a 256-CU part. Routing is exact (one-hot logits,
+    top-1); the two entry points give the same bits, and every row matches
+    the oracle."""
+    d, I, E = 256, 16384, 8
+    counts = [610 + 13 * i for i in range(E)]
+    T = sum(counts)
+    print(f"[gpu] gate/up walk with claimed last rounds: T={T}", flush=True)
+    wl = synth.make_custom(T=T, d=d, E=E, k=1, I=I, n_local=E, shadow_experts=[], gate="logits",
+                           seed=71, device=DEV)
+    rng = np.random.default_rng(71)
+    assign = rng.permutation(np.repeat(np.arange(E), counts))
+    logits = torch.zeros((T, E), dtype=torch.float32)
+    logits[torch.arange(T), torch.from_numpy(assign)] = 8.0
+    wl.logits = logits.to(DEV)
+    f = tg.EwForward(wl, keep_y=True)
+    f()
+    torch.cuda.synchronize()
+    assert np.array_equal(host(f.slot_counts), np.array(counts))
+    rows = host(f.pair_row)[:, 0]
+    y_fwd = u16(f.y[:T])
+    x_perm = torch.empty_like(wl.x)
+    x_perm[torch.from_numpy(rows).long().to(DEV)] = wl.x
+    h = torch.empty((T, I), dtype=torch.bfloat16, device=DEV)
+    y = torch.empty((T, d), dtype=torch.bfloat16, device=DEV)
+    tg.tg_expert_ffn_grouped(x_perm, f.slot_offsets, wl.S, T, wl.w13, wl.w2, d, I, h, y)
+    torch.cuda.synchronize()
+    assert np.array_equal(u16(y), y_fwd), "forward (claimed last rounds) vs standalone (static)"
+    off = host(f.slot_offsets)
+    xp = u16(x_perm)
+    for s_ in range(E):
+        a, b = int(off[s_]), int(off[s_ + 1])
+        ref_h, ref_y = O.expert_ffn(xp[a:b], u16(wl.w13[s_]), u16(wl.w2[s_]))
+        G.assert_close_bf16(u16(h[a:b]), ref_h, f"h slot {s_}")
+        G.assert_close_bf16(y_fwd[a:b], ref_y, f"y slot {s_}")
+
+
 @pytest.mark.parametrize("extra", [0, 1], ids=["half_round_spilled", "one_more_not_spilled"])
 def test_down_spill_threshold_edges_match_oracle(extra):
     """The down projection spills its partial last round when that round
