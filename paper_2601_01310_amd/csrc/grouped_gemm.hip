@@ -40,7 +40,8 @@
 // the host never reads them: 256 x 256 tiles with 4 waves (one per SIMD,
 // 128 x 128 each) for batches that fill the MFMA units, walked with the DMA
 // pipeline running on across tiles and results written straight from the
-// accumulators; or 32 x 256 tiles with 4 waves, where a launch mostly
+// accumulators; or 32-row tiles with 4 waves (32 x 256 in the gate/up
+// projection, 32 x 128 in the down projection), where a launch mostly
 // streams weights (decode steps, a single small expert batch) and a 256-row
 // tile would stage and multiply mostly zero rows (results staged through
 // each wave's own LDS region and written as 16-byte row segments). The
