@@ -122,6 +122,47 @@ def test_ffn_tile_shapes_give_identical_bits(tiny):
     G.assert_close_bf16(outs[0][1][o:o + 70], ref, "y slot 3")
 
 
+def test_small_tiles_with_partial_last_panels_give_identical_bits():
+    """d = 320 and I = 192, multiples of 64 but not of the panel widths: in
+    32-row tiles the down projection's last 128-column tile of a slot holds
+    64 valid columns and the one after it none, and the gate/up projection's
+    last panel is partial too. Forced 32-row tiles, forced 256-row tiles and
+    the launch's own choice give the same bits on ragged slots, and every
+    row matches the oracle."""
+    d, I = 320, 192
+    wl = synth.make_custom(T=64, d=d, E=8, k=2, I=I, n_local=8, shadow_experts=[0, 5],
+                           gate="weights", seed=23, device=DEV)
+    S = wl.S
+    cnt = torch.tensor([0, 33, 1, 70, 0, 64, 31, 40, 29, 32], dtype=torch.int32)
+    assert cnt.numel() == S
+    P = int(cnt.sum())
+    g = torch.Generator().manual_seed(9)
+    x_perm = torch.randn((P, d), generator=g).to(torch.bfloat16).to(DEV)
+    offsets = torch.zeros(S + 1, dtype=torch.int32)
+    offsets[1:] = torch.cumsum(cnt, 0)
+    off = offsets.numpy()
+    offsets = offsets.to(DEV)
+    outs = []
+    for policy in (tg.TILES_SMALL, tg.TILES_FULL, tg.TILES_AUTO):
+        h = torch.zeros((P, I), dtype=torch.bfloat16, device=DEV)
+        y = torch.zeros((P, d), dtype=torch.bfloat16, device=DEV)
+        with tg.tile_policy(policy):
+            tg.tg_expert_ffn_grouped(x_perm, offsets, S, P, wl.w13, wl.w2, d, I, h, y)
+        torch.cuda.synchronize()
+        outs.append((u16(h), u16(y)))
+    for o in outs[1:]:
+        assert np.array_equal(outs[0][0], o[0]), "h differs between tile shapes"
+        assert np.array_equal(outs[0][1], o[1]), "y differs between tile shapes"
+    xp = u16(x_perm)
+    for s_ in range(S):
+        a, b = int(off[s_]), int(off[s_ + 1])
+        if a == b:
+            continue
+        ref_h, ref_y = O.expert_ffn(xp[a:b], u16(wl.w13[s_]), u16(wl.w2[s_]))
+        G.assert_close_bf16(outs[0][0][a:b], ref_h, f"h slot {s_}")
+        G.assert_close_bf16(outs[0][1][a:b], ref_y, f"y slot {s_}")
+
+
 def test_tile_policy_rejects_unknown_values():
     with pytest.raises(tg.TgError):
         tg.tg_set_gemm_tile_policy(3)
