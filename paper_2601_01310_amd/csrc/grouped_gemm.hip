@@ -57,7 +57,7 @@
 // weight panel; each of the 8 XCDs (blocks are dealt to XCDs round robin)
 // takes one contiguous range of that order, keeping a panel in one L2. With
 // a schedule area (the fused forward and the replay have one), all but the
-// last three rounds of each range (at least three) are dealt statically and
+// last three rounds of each range (at least two) are dealt statically and
 // the rest are claimed from a per-XCD counter, blocks of an XCD that has run out taking tiles
 // from the other XCDs' counters, and the pieces of a spilled last round are
 // claimed from one more counter; the standalone FFN entry point, and 32-row
@@ -464,7 +464,7 @@ __global__ __launch_bounds__(256) void grouped_gemm_persistent4_kernel(
     const uint16_t* __restrict__ A, const int32_t* __restrict__ offsets, int S,
     const uint16_t* __restrict__ B, int K, int NW, int I, uint16_t* __restrict__ C, int ldc,
     int NT, const int32_t* __restrict__ perm, int kq, uint32_t kq_magic, int kq_shift,
-    int A_rows, int32_t* __restrict__ claims, unsigned long long* __restrict__ slots,
+    int A_rows, int32_t* __restrict__ claims,
     int policy) {
   constexpr int BM = 256, BN = 256, BK = 64, NWAVE = 4;
   constexpr int CH = BK / 8;                            // 16-byte chunks per staged row
@@ -532,53 +532,47 @@ __global__ __launch_bounds__(256) void grouped_gemm_persistent4_kernel(
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = wave >> 1, wn = wave & 1;
 
-    // Dynamic schedule (claims != nullptr; claims[0..8] and the slots are
-    // zero at launch). The first R rounds of each XCD's range are dealt
-    // statically (tile lo + jP + c is the block's tile j), R being all but
-    // the last three rounds and at least 3: blocks that start the same round
-    // together stream the same weight panels close together in time, so
-    // they share them in L2. Every later tile of XCD x's range is claimed
-    // from counter claims[x], position v giving tile lo_x + RP + v. A
-    // block whose own range is used up claims from the XCD with the most
-    // tiles left, so that XCDs that run ahead take work from those behind;
-    // every tile still runs exactly once, and its bits do not depend on where
-    // it runs. Tile j (j >= 3) of a block is claimed by thread 0 when the
-    // block starts its tile j - 3 (a static tile needs no claim; a block
-    // whose static tiles pass its range's end claims instead), published by
-    // wave 0 as (j, tile) in slot j % 2 of the block when that tile ends,
-    // loaded by every wave early in the last stage of tile j - 2 and used at
-    // the switch that follows (a wave that loads the slot before the record
-    // lands re-reads it). The
-    // claim and the slot load are plain memory instructions issued by every
-    // thread, with out-of-range offsets where they must do nothing (the
-    // resources are empty without a schedule), and their results are used
-    // only between tiles: no branch or loop makes the compiler wait for them
-    // inside the K loop, so the DMA pipeline never drains for the schedule.
+    // Dynamic schedule (claims != nullptr; claims[0..8] are zero at
+    // launch). The first R rounds of each XCD's range are dealt statically
+    // (tile lo + jP + c is the block's tile j), R being all but the last
+    // three rounds and at least 2: blocks that start the same round together
+    // stream the same weight panels close together in time, so they share
+    // them in L2. Every later tile of XCD x's range is claimed from counter
+    // claims[x], position v giving tile lo_x + RP + v. A block whose own
+    // range is used up claims from the XCD with the most tiles left, so that
+    // XCDs that run ahead take work from those behind; every tile still runs
+    // exactly once, and its bits do not depend on where it runs. Tile j of a
+    // block is claimed by thread 0 when the block starts its tile j - 2 (a
+    // static tile needs no claim; a block whose static tiles pass its range's
+    // end claims instead); when tile j - 2 ends, wave 0 resolves the claim
+    // and hands tile j to the other waves through LDS, at the switch that
+    // makes it the next tile. The claim is a plain memory instruction issued
+    // by every thread, with an out-of-range offset where it must do nothing
+    // (the resource is empty without a schedule), and its result is read
+    // only after the tile's last stage, whose wait has covered it: no branch
+    // or loop makes the compiler wait for it inside the K loop, so the DMA
+    // pipeline never drains for the schedule.
     const bool dyn = claims != nullptr;
     const int P = per_xcd_blocks;
     constexpr int kOut = (int)0x80000000u;  // an offset past any resource: no access
     constexpr int kCoherent = 16;           // sc1: the device-coherent copy
     const __amdgpu_buffer_rsrc_t cl_rsrc = make_rsrc(claims, dyn ? kXcds * 4 : 0);
-    const __amdgpu_buffer_rsrc_t sl_rsrc =
-        make_rsrc(dyn ? static_cast<const void*>(slots + 2 * blockIdx.x) : nullptr, dyn ? 16 : 0);
     auto range_lo = [&](int xx) { return xx * per; };
     auto range_hi = [&](int xx) { return min(xx * per + per, n_head); };
     int cl_x = x, cl_v = 0;        // thread 0: the counter claimed from, its last value
     int cl_last = -1;              // wave 0: the block's latest known tile (-1: none left)
-    unsigned long long slot_v = 0; // the slot as loaded in the last stage of a tile
-    // Read right after the last stage, whose wait has covered both loads, so
-    // that nothing later waits for them: thread 0's claim and the slot.
-    int cl_got = 0, slot_tile = 0, slot_seq = 0;
-    // Tile j + 3's claim, issued when tile j starts (thread 0 only).
-    const int R = max(3, (per + P - 1) / P - kDynRounds);  // static rounds
+    // Read right after the last stage, whose wait has covered the claim, so
+    // that nothing later waits for it: thread 0's claim.
+    int cl_got = 0;
+    // Tile j + 2's claim, issued when tile j starts (thread 0 only).
+    const int R = max(2, (per + P - 1) / P - kDynRounds);  // static rounds
     auto static_tile = [&](int j) { return j < R && lo + j * P + c < hi; };
     auto claim_issue = [&](int j) {
       cl_v = __builtin_amdgcn_raw_ptr_buffer_atomic_add_i32(
-          1, cl_rsrc, (tid == 0 && cl_last >= 0 && !static_tile(j + 3)) ? cl_x * 4 : kOut, 0, 0);
+          1, cl_rsrc, (tid == 0 && cl_last >= 0 && !static_tile(j + 2)) ? cl_x * 4 : kOut, 0, 0);
     };
-    // When tile j ends: resolve tile j + 3's claim and publish it (wave 0).
-    auto claim_publish = [&](int jn) {
-      if (wave != 0) return;
+    // When tile j ends: tile j + 2, static or from the claim (wave 0).
+    auto claim_resolve = [&](int jn) -> int {
       int t = -1;
       if (cl_last >= 0 && static_tile(jn)) {
         t = lo + jn * P + c;
@@ -614,21 +608,7 @@ __global__ __launch_bounds__(256) void grouped_gemm_persistent4_kernel(
         }
       }
       cl_last = t;
-      typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
-      const u32x2 rec = {(unsigned int)t, (unsigned int)jn};
-      __builtin_amdgcn_raw_buffer_store_b64(rec, sl_rsrc, lane == 0 ? (jn & 1) * 8 : kOut, 0,
-                                            kCoherent);
-    };
-    // At the switch after tile j - 2: tile j, from the slot loaded in that
-    // tile's last stage.
-    auto claim_result = [&](int jn) -> int {
-      if (slot_seq == jn) return slot_tile;
-      unsigned long long v;
-      do {  // the record had not landed when the slot was read
-        v = __hip_atomic_load(&slots[2 * blockIdx.x + (jn & 1)], __ATOMIC_RELAXED,
-                              __HIP_MEMORY_SCOPE_AGENT);
-      } while ((unsigned int)(v >> 32) != (unsigned int)jn);
-      return __builtin_amdgcn_readfirstlane((int)(unsigned int)v);
+      return t;
     };
 
     int s_cur = 0, before = 0, pos = 0, c_nt = 0, c_m = 0;
@@ -800,11 +780,8 @@ __global__ __launch_bounds__(256) void grouped_gemm_persistent4_kernel(
     a_offsets(row0, rows, a_off);
     int Ln = L + per_xcd_blocks;
     bool has_n = Ln < hi;
-    // The block's tile 2 (static; run only after tile 1).
-    const int t2_static = (has_n && Ln + P < hi) ? Ln + P : -1;
-    if (dyn) cl_last = t2_static;
-    int tj = 0;        // index of the current tile in this block's sequence
-    int slot_off = 0;  // byte offset of the slot read in this tile's last stage: (tj + 2) % 2
+    if (dyn) cl_last = has_n ? Ln : -1;  // tile 1
+    int tj = 0;  // index of the current tile in this block's sequence
     int slot_n = slot, row0_n = row0, rows_n = rows, nt_n = nt;
     if (has_n) seek(Ln, slot_n, row0_n, rows_n, nt_n);
     __amdgpu_buffer_rsrc_t a_n = a_of(row0_n, rows_n), b_n = b_of(slot_n, nt_n);
@@ -844,10 +821,7 @@ __global__ __launch_bounds__(256) void grouped_gemm_persistent4_kernel(
       // barrier (the next tile may run in another mode).
 #define TG_STAGE(kt, LAST)                                                                 \
   do {                                                                                     \
-    TG_TARGETS(kt, LAST);                                                                        \
-    if constexpr (LAST)                                                                    \
-      slot_v = __builtin_bit_cast(unsigned long long, __builtin_amdgcn_raw_buffer_load_b64(  \
-                                                          sl_rsrc, slot_off, 0, kCoherent)); \
+    TG_TARGETS(kt, LAST);                                                                  \
     TG_FRAGS(ab, bb, 1, 1);                                                                \
     TG_ISSUE_A(ra, offa, ka * BK, abn, 0, AI / 2);                                        \
     TG_MFMAS(0, 0, NQ);                                                                    \
@@ -885,8 +859,6 @@ __global__ __launch_bounds__(256) void grouped_gemm_persistent4_kernel(
       for (int kt = 0; kt < nk - 1; ++kt) TG_STAGE(kt, false);  // nk >= 2
       TG_STAGE(nk - 1, true);
       cl_got = __builtin_amdgcn_readfirstlane(cl_v);  // thread 0's claim in wave 0
-      slot_tile = __builtin_amdgcn_readfirstlane((int)(unsigned int)slot_v);
-      slot_seq = __builtin_amdgcn_readfirstlane((int)(unsigned int)(slot_v >> 32));
 #undef TG_STAGE
       // acc[nb][mb] register r of lane l: row mb*32 + l%32, column
       // nb*32 + 8*(r/4) + 4*(l/32) + r%4 of the wave's sub-tile; SwiGLU pairs
@@ -928,8 +900,26 @@ __global__ __launch_bounds__(256) void grouped_gemm_persistent4_kernel(
       if (rows > 128) run_tile(std::integral_constant<int, 0>{});
       else if (rows > 64) run_tile(std::integral_constant<int, 1>{});
       else run_tile(std::integral_constant<int, 2>{});
-      if (dyn) claim_publish(tj + 3);
       if (!has_n) break;
+      // Tile tj + 2 becomes the next tile at this switch. With a schedule
+      // wave 0 resolves it and hands it to the other waves through the A
+      // stage buffer that the last stage released (the next tile's first
+      // stage refills it only after the second barrier).
+      int t2;
+      if (dyn) {
+        int* const rec = reinterpret_cast<int*>(smem + (ab ^ 1) * A_ST);
+        if (wave == 0) {
+          const int t = claim_resolve(tj + 2);
+          if (lane == 0) *rec = t;
+        }
+        __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): the record is written
+        block_barrier();
+        t2 = __builtin_amdgcn_readfirstlane(*rec);
+        __builtin_amdgcn_s_waitcnt(0xc07f);  // and read by every wave
+        block_barrier();
+      } else {
+        t2 = Ln + per_xcd_blocks < hi ? Ln + per_xcd_blocks : -1;
+      }
       row0 = row0_n;
       rows = rows_n;
       nt = nt_n;
@@ -937,15 +927,9 @@ __global__ __launch_bounds__(256) void grouped_gemm_persistent4_kernel(
       b_cur = b_n;
 #pragma unroll
       for (int i = 0; i < AI; ++i) a_off[i] = a_off_n[i];
-      if (dyn) {
-        Ln = (tj == 0) ? t2_static : claim_result(tj + 2);
-        has_n = Ln >= 0;
-      } else {
-        Ln += per_xcd_blocks;
-        has_n = Ln < hi;
-      }
+      Ln = t2;
+      has_n = Ln >= 0;
       ++tj;
-      slot_off = (tj & 1) * 8;
       if (has_n) {
         seek(Ln, slot_n, row0_n, rows_n, nt_n);
         a_n = a_of(row0_n, rows_n);
@@ -1040,10 +1024,10 @@ hipError_t launch_persistent4(const uint16_t* A, const int32_t* offsets, int S, 
   while ((1 << l) < kq) ++l;
   const uint32_t m = (uint32_t)((((uint64_t)1 << (31 + l)) + (uint64_t)kq - 1) / (uint64_t)kq);
   const int grid = std::max(kXcds, cu_count() / kXcds * kXcds);  // a multiple of 8, never 0
-  const bool dyn = sched && sched->claims && grid <= kSchedMaxBlocks;
+  const bool dyn = sched && sched->claims;
   hipLaunchKernelGGL((grouped_gemm_persistent4_kernel<SWIGLU, GATHER, TAIL>), dim3(grid), dim3(256),
                      0, stream, A, offsets, S, B, K, NW, I, C, ldc, NT, perm, kq, m, l, A_rows,
-                     dyn ? sched->claims : nullptr, dyn ? sched->slots : nullptr,
+                     dyn ? sched->claims : nullptr,
                      g_tile_policy.load(std::memory_order_relaxed));
   return hipGetLastError();
 }

@@ -10,7 +10,7 @@
 // address resolved once per device with hipGetSymbolAddress, never the name.
 // Nothing in the forward's workspace has to start at zero when the call is
 // made: every kernel writes what a later kernel reads, and what must be zero
-// when a kernel starts (the grouped GEMMs' tile counters and claim slots) is
+// when a kernel starts (the grouped GEMMs' tile counters) is
 // cleared by the forward's own dispatch kernels, so the host never clears
 // the area.
 #include <hip/hip_runtime.h>

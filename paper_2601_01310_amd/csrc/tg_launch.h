@@ -22,22 +22,17 @@ tg_status set_error(tg_status s, const char* fmt, ...);
 // Work area of the dynamic tile schedule of the two grouped GEMMs of one
 // forward (or replay): per GEMM, 16 claim counters (one per XCD for the
 // tile walk, then one for the pieces of a spilled last round; the rest
-// unused) and two 8-byte publication slots per block. The dispatch of the same call
-// zeroes the whole area before the GEMMs run.
-constexpr int kSchedMaxBlocks = 1024;
+// unused). The dispatch of the same call zeroes the whole area before the
+// GEMMs run.
 struct GemmSched {
   int32_t* claims;
-  unsigned long long* slots;
 };
-constexpr size_t kSchedSlotBytes = 2 * kSchedMaxBlocks * sizeof(unsigned long long);
-constexpr size_t kSchedBytes = 2 * (16 * sizeof(int32_t) + kSchedSlotBytes);
+constexpr size_t kSchedBytes = 2 * 16 * sizeof(int32_t);
 // Carves the two GEMMs' schedules out of a kSchedBytes area (base may be null).
 inline void sched_carve(void* base, GemmSched* gateup, GemmSched* down) {
   char* b = static_cast<char*>(base);
   gateup->claims = b ? reinterpret_cast<int32_t*>(b) : nullptr;
   down->claims = b ? reinterpret_cast<int32_t*>(b + 64) : nullptr;
-  gateup->slots = b ? reinterpret_cast<unsigned long long*>(b + 128) : nullptr;
-  down->slots = b ? reinterpret_cast<unsigned long long*>(b + 128 + kSchedSlotBytes) : nullptr;
 }
 
 hipError_t launch_gate_topk(const uint16_t* x, const uint16_t* wg, const float* logits_in, int T,
