@@ -610,20 +610,7 @@ def measure_workload(wl, alive, steps, warmup, with_failover=True):
                     "routed_pairs": fo_pairs, "blocks": FAILOVER_BLOCKS, "steps_per_block": n}
 
     d, I = wl.d, wl.I
-    gemm1_flop = 4.0 * d * I * P
-    gemm1_s = stage_ms[2] * 1e-3
-    # Algorithmic bytes of the gate/up GEMM: the touched slots' W1/W3, the
-    # routed rows of x and h.
-    gemm1_bytes = touched * 2.0 * I * d * 2 + P * d * 2.0 + P * I * 2.0
-    if gemm1_flop / max(gemm1_bytes, 1.0) >= RIDGE_FLOP_PER_BYTE:
-        achieved = gemm1_flop / gemm1_s / 1e12
-        roof = {"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
-                "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS}
-    else:
-        achieved = gemm1_bytes / gemm1_s / 1e9
-        roof = {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                "frac": achieved / PEAK_HBM_GBS}
-    roof = {"bound": roof["bound"], "kernel": "grouped_gemm gate/up + SwiGLU", **roof}
+    roof = gateup_roofline(d, I, P, touched, stage_ms[2] * 1e-3)
     p50 = step_ev[len(step_ev) // 2]
     # Bytes the whole step must stream: every touched slot's three weight
     # matrices, the token rows and the outputs.
@@ -635,6 +622,27 @@ def measure_workload(wl, alive, steps, warmup, with_failover=True):
             "step_flop_frac": 6.0 * d * I * P / (p50 * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
             "step_hbm_frac": step_bytes / (p50 * 1e-3) / 1e9 / PEAK_HBM_GBS,
             "failover": failover}
+
+
+def gateup_roofline(d, I, pairs, touched, seconds):
+    """Roofline entry of the gate/up GEMM from its average launch time.
+
+    Algorithmic flops 4·d·I per routed pair; algorithmic bytes the touched
+    slots' W1/W3 (2·I·d bf16 each) plus the routed rows of x and h. At or
+    above the ridge point (peak flops over peak bytes) the GEMM is reported
+    against the bf16 MFMA peak, below it against HBM.
+    """
+    flop = 4.0 * d * I * pairs
+    nbytes = touched * 2.0 * I * d * 2 + pairs * d * 2.0 + pairs * I * 2.0
+    if flop / max(nbytes, 1.0) >= RIDGE_FLOP_PER_BYTE:
+        achieved = flop / seconds / 1e12
+        roof = {"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
+                "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS}
+    else:
+        achieved = nbytes / seconds / 1e9
+        roof = {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": achieved / PEAK_HBM_GBS}
+    return {"bound": roof["bound"], "kernel": "grouped_gemm gate/up + SwiGLU", **roof}
 
 
 def compact(wl, r):

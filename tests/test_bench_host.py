@@ -46,3 +46,22 @@ def test_kernel_source_hash_ignores_comments_but_not_code(tmp_path):
     assert bench.kernel_source_hash([str(a)]) == h0
     a.write_text("int f(int x) {\n  return x + 2;\n}\n")
     assert bench.kernel_source_hash([str(a)]) != h0
+
+
+def test_gateup_roofline_picks_the_bound_by_arithmetic_intensity():
+    """The mixtral batch (8192 pairs, 8 touched slots) is past the ridge
+    point and is reported against the bf16 MFMA peak; the decode batch (116
+    pairs over 32 touched slots) streams weights and is reported against HBM,
+    with the algorithmic bytes written out by hand."""
+    r = bench.gateup_roofline(4096, 14336, 8192, 8, 1.5e-3)
+    flop = 4.0 * 4096 * 14336 * 8192
+    assert r["bound"] == "mfma" and r["unit"] == "TFLOP/s"
+    assert abs(r["achieved"] - flop / 1.5e-3 / 1e12) < 1e-9
+    assert abs(r["frac"] - r["achieved"] / 2500.0) < 1e-12
+    d, I, P, touched = 7168, 2048, 116, 32
+    r = bench.gateup_roofline(d, I, P, touched, 305e-6)
+    weights = 32 * 4096 * 7168 * 2          # W1 and W3 of every touched slot
+    rows = 116 * 7168 * 2 + 116 * 2048 * 2  # routed rows of x read, of h written
+    assert r["bound"] == "hbm" and r["unit"] == "GB/s"
+    assert abs(r["achieved"] - (weights + rows) / 305e-6 / 1e9) < 1e-6
+    assert abs(r["frac"] - r["achieved"] / 8000.0) < 1e-12
