@@ -576,6 +576,87 @@ def test_seeded_random_sweep_matches_oracle(case):
         assert np.array_equal(f["out"], g["out"]), "fused differs from stepwise"
 
 
+def _ragged_cases(seed, n):
+    """Slot populations of four kinds: decode-like (0-39 rows), within three
+    rows of a multiple of 256, heavy-tailed (Pareto), and uniform up to 1500;
+    T x max(d, I) kept under 2e8 elements."""
+    rng = np.random.default_rng(seed)
+    out = []
+    for _ in range(n):
+        E = int(rng.integers(1, 65))
+        d = int(rng.choice([128, 256, 320, 512, 768, 1024, 1536, 2048, 4096]))
+        I = int(rng.integers(2, 129)) * 64
+        while E * 3 * I * d > 6e8:
+            I = max(128, I // 128 * 64)
+            if I == 128 and E * 3 * I * d > 6e8:
+                E = max(1, E // 2)
+        kind = int(rng.integers(0, 4))
+        if kind == 0:
+            counts = rng.integers(0, 40, size=E)
+        elif kind == 1:
+            counts = 256 * rng.integers(0, 5, size=E) + rng.integers(-3, 4, size=E)
+        elif kind == 2:
+            counts = (rng.pareto(1.2, size=E) * 300).astype(int)
+        else:
+            counts = rng.integers(0, 1500, size=E)
+        counts = np.clip(counts, 0, 4000).astype(int)
+        while counts.sum() * max(I, d) > 2e8:
+            counts = counts // 2
+        if counts.sum() == 0:
+            counts[rng.integers(0, E)] = 1
+        out.append((E, d, I, tuple(int(c) for c in counts), int(rng.integers(0, 3)),
+                    int(rng.integers(1 << 30))))
+    return out
+
+
+@pytest.mark.parametrize("case", _ragged_cases(5, 12),
+                         ids=lambda c: f"E{c[0]}_d{c[1]}_I{c[2]}_T{sum(c[3])}_pol{c[4]}")
+def test_ragged_slot_populations_give_identical_bits_under_every_schedule(case):
+    """Seeded slot populations of up to 64 slots and 4000 rows each, with the
+    routing forced (one-hot logits, top-1). The fused forward (its tile
+    policy drawn per case; the last rounds of large launches claimed from
+    counters) and the standalone FFN under each of the three tile policies
+    (every tile dealt statically) give the same bits; sampled rows of four
+    slots, the first and last row of each included, match the oracle."""
+    E, d, I, counts, pol, seed = case
+    T = sum(counts)
+    print(f"[gpu] ragged case E={E} d={d} I={I} T={T} policy={pol}", flush=True)
+    wl = synth.make_custom(T=T, d=d, E=E, k=1, I=I, n_local=E, shadow_experts=[], gate="logits",
+                           seed=seed, device=DEV)
+    rng = np.random.default_rng(seed)
+    assign = rng.permutation(np.repeat(np.arange(E), counts))
+    logits = torch.zeros((T, E), dtype=torch.float32)
+    logits[torch.arange(T), torch.from_numpy(assign)] = 8.0
+    wl.logits = logits.to(DEV)
+    with tg.tile_policy(pol):
+        f = tg.EwForward(wl, keep_y=True)
+        f()
+        torch.cuda.synchronize()
+    assert np.array_equal(host(f.slot_counts), np.array(counts))
+    rows = host(f.pair_row)[:, 0]
+    y_fwd = u16(f.y[:T])
+    x_perm = torch.empty_like(wl.x)
+    x_perm[torch.from_numpy(rows).long().to(DEV)] = wl.x
+    h = torch.empty((T, I), dtype=torch.bfloat16, device=DEV)
+    y = torch.empty((T, d), dtype=torch.bfloat16, device=DEV)
+    for p2 in (tg.TILES_AUTO, tg.TILES_SMALL, tg.TILES_FULL):
+        with tg.tile_policy(p2):
+            y.zero_()
+            tg.tg_expert_ffn_grouped(x_perm, f.slot_offsets, wl.S, T, wl.w13, wl.w2, d, I, h, y)
+            torch.cuda.synchronize()
+        assert np.array_equal(u16(y), y_fwd), f"forward (policy {pol}) vs standalone (policy {p2})"
+    off = host(f.slot_offsets)
+    xp, H = u16(x_perm), u16(h)
+    for s_ in rng.choice(E, size=min(E, 4), replace=False):
+        a, b = int(off[s_]), int(off[s_ + 1])
+        if b == a:
+            continue
+        pick = np.unique(np.concatenate([[a, b - 1], rng.integers(a, b, size=6)]))
+        ref_h, ref_y = O.expert_ffn(xp[pick], u16(wl.w13[s_]), u16(wl.w2[s_]))
+        G.assert_close_bf16(H[pick], ref_h, f"h slot {s_}")
+        G.assert_close_bf16(y_fwd[pick], ref_y, f"y slot {s_}")
+
+
 def test_empty_batch():
     wl = synth.make_custom(T=4, d=256, E=8, k=2, I=128, n_local=8, shadow_experts=[],
                            gate="weights", seed=5, device=DEV)
