@@ -39,8 +39,9 @@
 // in one of two shapes, chosen on the device from the slot counts, so that
 // the host never reads them: 256 x 256 tiles with 4 waves (one per SIMD,
 // 128 x 128 each) for batches that fill the MFMA units, walked with the DMA
-// pipeline running on across tiles and results written straight from the
-// accumulators; or 32-row tiles with 4 waves (32 x 256 in the gate/up
+// pipeline running on across tiles (the gate/up results written straight
+// from the accumulators, the down projection's staged in LDS and written as
+// whole 128-byte lines); or 32-row tiles with 4 waves (32 x 256 in the gate/up
 // projection, 32 x 128 in the down projection), where a launch mostly
 // streams weights (decode steps, a single small expert batch) and a 256-row
 // tile would stage and multiply mostly zero rows (results staged through
@@ -48,9 +49,9 @@
 // 32-row shape runs when its rounds of tiles over the grid cost less, at
 // about two thirds of a 256-row round each; in the down projection, whose
 // partial last round of 256 x 256 tiles runs as 128 x 128 quarter tiles
-// (keeping the CUs busy with few tiles), only when no slot holds more than
-// 32 rows and the 32-row tiles fill more than one round. All shapes give
-// identical bits, so the choice never changes a result.
+// (keeping the CUs busy with few tiles), when no slot holds more than 32
+// rows or the 32-row tiles fit in one round. All shapes give identical
+// bits, so the choice never changes a result.
 //
 // Tile order: the tiles of one launch are enumerated slot by slot, then by
 // weight panel (n), then by row block (m), so consecutive tiles share a
@@ -99,6 +100,8 @@ __device__ __forceinline__ void block_barrier() {
 }
 
 typedef __attribute__((address_space(3))) uint16_t lds_u16;
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 // SwiGLU of one output element: silu(g) * u = g / (1 + e^-g) * u, with the
 // reciprocal from the hardware approximation (about 1 ulp in float32, far
@@ -483,14 +486,17 @@ __global__ __launch_bounds__(256) void grouped_gemm_persistent4_kernel(
   const Census cs = census(offsets, S, NT);
   bool small_tiles = policy == kTilesSmall;
   if (policy == kTilesAuto) {
-    // Rounds of tiles over the grid at each height; a 32-row round costs
-    // about two thirds of a 256-row round (it streams the same weight panel
-    // with an eighth of the MFMA work). With the quarter split of a partial
-    // last round (TAIL) the 256-row walk keeps the CUs busy even with few
-    // tiles; there 32-row tiles pay only when no slot exceeds 32 rows and
-    // they fill more than one round.
+    // Gate/up: rounds of tiles over the grid at each height; a 32-row round
+    // costs about two thirds of a 256-row round (it streams the same weight
+    // panel with an eighth of the MFMA work). Down (TAIL, 32 x 128 tiles, two
+    // per 256-column panel): 32-row tiles when no slot exceeds 32 rows, or
+    // when they fit in one round; otherwise the 256-row walk, whose partial
+    // last round splits into quarters, is faster (measured on single expert
+    // batches: a Mixtral expert's down projection of 64 to 256 rows takes
+    // 88 us in one round of 32-row tiles against 107-139 us in 256-row
+    // tiles, and 170 against 139 us at 512 rows, two rounds).
     const int rs = (cs.small + G - 1) / G, rf = (cs.full + G - 1) / G;
-    small_tiles = TAIL ? (cs.max_rows <= 32 && cs.small > G) : 2 * rs < 3 * rf;
+    small_tiles = TAIL ? (cs.max_rows <= 32 || 2 * cs.small <= G) : 2 * rs < 3 * rf;
   }
   if (small_tiles) {
     // 32 x 256 tiles (gate/up) or 32 x 128 tiles (down), each XCD walking
@@ -864,25 +870,74 @@ __global__ __launch_bounds__(256) void grouped_gemm_persistent4_kernel(
       // nb*32 + 8*(r/4) + 4*(l/32) + r%4 of the wave's sub-tile; SwiGLU pairs
       // gate block nb with up block nb + NBm/2.
       const int colbase = SWIGLU ? nt * (BN / 2) + cw : nt * BN + cw;
+      if constexpr (SWIGLU) {
 #pragma unroll
-      for (int mb = 0; mb < MBm; ++mb) {
-        const int r = rbase + mb * 32 + (lane & 31);
-        uint16_t* crow = C + (size_t)(row0 + r) * ldc + colbase + 4 * (lane >> 5);
+        for (int mb = 0; mb < MBm; ++mb) {
+          const int r = rbase + mb * 32 + (lane & 31);
+          uint16_t* crow = C + (size_t)(row0 + r) * ldc + colbase + 4 * (lane >> 5);
 #pragma unroll
-        for (int nb = 0; nb < (SWIGLU ? NBm / 2 : NBm); ++nb) {
+          for (int nb = 0; nb < NBm / 2; ++nb) {
 #pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            float v[4];
+            for (int q = 0; q < 4; ++q) {
+              float v[4];
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              const int rr = 4 * q + e;
-              v[e] = SWIGLU ? swiglu(acc[nb][mb][rr], acc[nb + NBm / 2][mb][rr]) : acc[nb][mb][rr];
+              for (int e = 0; e < 4; ++e) {
+                const int rr = 4 * q + e;
+                v[e] = swiglu(acc[nb][mb][rr], acc[nb + NBm / 2][mb][rr]);
+              }
+              uint2 pk;
+              pk.x = pack_bf16x2(v[0], v[1]);
+              pk.y = pack_bf16x2(v[2], v[3]);
+              if (r < rows && colbase + 4 * (lane >> 5) + nb * 32 + 8 * q < ldc)
+                *reinterpret_cast<uint2*>(crow + nb * 32 + 8 * q) = pk;
             }
-            uint2 pk;
-            pk.x = pack_bf16x2(v[0], v[1]);
-            pk.y = pack_bf16x2(v[2], v[3]);
-            if (r < rows && colbase + 4 * (lane >> 5) + nb * 32 + 8 * q < ldc)
-              *reinterpret_cast<uint2*>(crow + nb * 32 + 8 * q) = pk;
+          }
+        }
+      } else {
+        // The down projection's rows leave as whole 128-byte lines: each
+        // 32-row by 64-column block of the wave's sub-tile is staged in the
+        // wave's own quarter of the A buffer that the last stage released
+        // (the part that only this wave's next A loads refill, issued after
+        // these reads; rows padded by 16 bytes against bank conflicts) and
+        // read back as 16-byte pieces of whole rows, eight rows per store.
+        // Straight from the accumulators each store would put 16 bytes into
+        // each of 32 rows; staged, the DeepSeek-sized down GEMM runs 7-8 %
+        // faster. (The gate/up GEMM gains nothing from staging: its cost
+        // there is the SwiGLU arithmetic.) The stores go through a resource
+        // over the tile's rows, so rows past its end are dropped by the
+        // hardware's range check.
+        constexpr int PITCH = 64 + 8;  // staged row pitch (elements)
+        static_assert(32 * PITCH <= A_ST / NWAVE, "staging fits in the wave's quarter");
+        lds_u16* const region = smem3 + (ab ^ 1) * A_ST + wave * (A_ST / NWAVE);
+        lds_u16* const wbase = region + (lane & 31) * PITCH + 4 * (lane >> 5);
+        lds_u16* const rbase_l = region + (lane >> 3) * PITCH + (lane & 7) * 8;
+        const __amdgpu_buffer_rsrc_t c_rsrc =
+            make_rsrc(C + (size_t)row0 * ldc, (uint32_t)rows * ldc * 2);
+#pragma unroll
+        for (int hb = 0; hb < NBm / 2; ++hb) {
+          const int col = colbase + hb * 64 + (lane & 7) * 8;
+          const int voff0 = col < ldc ? ((rbase + (lane >> 3)) * ldc + col) * 2 : kOut;
+#pragma unroll
+          for (int mb = 0; mb < MBm; ++mb) {
+#pragma unroll
+            for (int n2 = 0; n2 < 2; ++n2) {
+#pragma unroll
+              for (int q = 0; q < 4; ++q) {
+                const f32x16& a = acc[2 * hb + n2][mb];
+                const u32x2 pk = {pack_bf16x2(a[4 * q], a[4 * q + 1]),
+                                  pack_bf16x2(a[4 * q + 2], a[4 * q + 3])};
+                *reinterpret_cast<__attribute__((address_space(3))) u32x2*>(
+                    wbase + n2 * 32 + 8 * q) = pk;
+              }
+            }
+            __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const u32x4 v = *reinterpret_cast<const __attribute__((address_space(3))) u32x4*>(
+                  rbase_l + i * 8 * PITCH);
+              const int voff = voff0 == kOut ? kOut : voff0 + (mb * 32 + i * 8) * ldc * 2;
+              __builtin_amdgcn_raw_buffer_store_b128(v, c_rsrc, voff, 0, 0);
+            }
           }
         }
       }
