@@ -902,8 +902,8 @@ __global__ __launch_bounds__(256) void grouped_gemm_persistent4_kernel(
         // read back as 16-byte pieces of whole rows, eight rows per store.
         // Straight from the accumulators each store would put 16 bytes into
         // each of 32 rows; staged, the DeepSeek-sized down GEMM runs 7-8 %
-        // faster. (The gate/up GEMM gains nothing from staging: its cost
-        // there is the SwiGLU arithmetic.) The stores go through a resource
+        // faster; the gate/up GEMM's output gains nothing from the same
+        // staging, so it keeps its direct stores. The stores go through a resource
         // over the tile's rows, so rows past its end are dropped by the
         // hardware's range check.
         constexpr int PITCH = 64 + 8;  // staged row pitch (elements)
